@@ -1,0 +1,124 @@
+/*
+ * cartpole.h -- C ABI of libcartpole.so: the batched cart-pole environment
+ * step on an AMD Instinct MI355X (gfx950), at three fusion levels.
+ *
+ * The operation is the environment update step of the paper's case study
+ * ("Operator Fusion in XLA: Analysis and Evaluation", Sec. "Case Study on
+ * Cart-pole"): for every environment of a batch, one explicit-Euler step of
+ * the frictionless cart-pole dynamics under a +-10 N push, reward 1, the
+ * termination test (|x| > 2.4 or |theta| > 12 degrees) and, on termination,
+ * an automatic reset to a random start state.  Random actions and random
+ * start states (Sec. "Remove cuRAND Kernels") come from the counter-based
+ * Threefry-2x32-20 generator keyed by (seed, environment, step) and
+ * (seed, environment, episode), so results do not depend on launch shape,
+ * batch split or fusion level.  The three levels follow the paper's
+ * evaluation (Sec. "Evaluations"): an unfused chain of one-operation kernels
+ * (its eager baseline), one fused kernel per step (its "no concat" fully
+ * fused kernel) and one kernel for many steps with the state held in
+ * registers (its unrolled scan and the hand-written CUDA kernel).
+ *
+ * Conventions shared by every entry point:
+ *  - Every pointer inside cp_states / cp_traj is a DEVICE pointer owned by the
+ *    caller; the library never allocates, frees or retains memory.
+ *  - Calls are asynchronous on s->stream (a hipStream_t; NULL = the null
+ *    stream).  Results are visible after the caller synchronises it.
+ *  - Return value: CP_OK (0) or a negative CP_ERR_* code; cp_last_error()
+ *    then gives a message (per calling thread).  Arguments are validated
+ *    before any HIP call: on CP_ERR_NULL/SIZE/ALIGN/RANGE/UNSUPPORTED nothing
+ *    is launched and *s is unchanged.  CP_ERR_HIP reports a failed launch.
+ *  - Outputs must not overlap the state arrays or each other.
+ *  - A cp_states handle is not thread-safe; distinct handles are independent.
+ */
+#ifndef CARTPOLE_H
+#define CARTPOLE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Fusion levels (cp_states.variant). */
+#define CP_UNFUSED 0  /* one kernel per primitive operation, temporaries in HBM      */
+#define CP_FUSED 1    /* one kernel per step, state read and written once per step  */
+#define CP_RESIDENT 2 /* one kernel per rollout, state held in registers            */
+
+#define CP_OK 0
+#define CP_ERR_NULL (-1)        /* a required pointer is NULL                          */
+#define CP_ERR_SIZE (-2)        /* n, n_steps or workspace size out of range          */
+#define CP_ERR_ALIGN (-3)       /* a device pointer is not 4-byte aligned (u8: any)   */
+#define CP_ERR_RANGE (-4)       /* step counter or environment index would overflow   */
+#define CP_ERR_HIP (-5)         /* a HIP launch failed; see cp_last_error()           */
+#define CP_ERR_UNSUPPORTED (-6) /* combination not provided (e.g. policy + UNFUSED)    */
+
+#define CP_POLICY_WEIGHTS 4480 /* bf16 values: W1[4][64], W2[64][64], W3[64][2]       */
+#define CP_MAX_STEPS ((uint64_t)1 << 31) /* t + n_steps must stay below this       */
+
+/* Batch state, structure of arrays.  Environment i has global index
+ * env_base + i: that index keys its random actions and reset states, so a
+ * batch split into several handles reproduces the undivided batch exactly. */
+typedef struct cp_states {
+    float *x, *x_dot, *theta, *theta_dot; /* [n] each, binary32                     */
+    uint32_t *ep_index; /* [n] episodes completed since cp_init (keys the reset)   */
+    uint32_t *ep_len;   /* [n] steps (= return) of the running episode             */
+    int64_t n;          /* number of environments, 1 <= n <= 2^31 - 1              */
+    uint32_t env_base;  /* global index of environment 0; env_base + n <= 2^32     */
+    int32_t variant;    /* CP_UNFUSED, CP_FUSED or CP_RESIDENT                     */
+    uint64_t seed;      /* set by cp_init: seed of the reset stream                */
+    uint64_t t;         /* global step counter, advanced by cp_step / cp_rollout   */
+    void *stream;       /* hipStream_t the calls are queued on                     */
+    const uint16_t *policy_w; /* NULL = random actions; else CP_POLICY_WEIGHTS bf16
+                                 bit patterns of the MLP policy (device memory)    */
+    void *workspace;          /* CP_UNFUSED temporaries, >= cp_workspace_bytes()  */
+    size_t workspace_bytes;
+} cp_states;
+
+/* Rollout outputs; every field may be NULL (= not produced).  Arrays are
+ * step-major: obs[t][4][n] (x, x_dot, theta, theta_dot after step t, after
+ * any reset), reward[t][n], done[t][n] (1 on a terminating step).  Per
+ * environment, over this rollout: done_count, total_reward (the sum of the
+ * rewards), ret_sum (sum of the returns of the episodes that ended in it).
+ * global[0] += total terminations, global[1] += sum of those returns (the
+ * caller clears global before the first call it wants counted).            */
+typedef struct cp_traj {
+    float *obs;
+    float *reward;
+    uint8_t *done;
+    uint32_t *done_count;
+    float *total_reward;
+    uint32_t *ret_sum;
+    unsigned long long *global;
+} cp_traj;
+
+/* Reset every environment to the start state of episode 0 drawn from the
+ * reset stream of `seed`; clears ep_index and ep_len; sets s->seed = seed
+ * and s->t = 0.  Needs the state arrays only.                               */
+int cp_init(cp_states *s, uint64_t seed);
+
+/* One step of every environment at global step s->t, then s->t += 1.
+ * actions: device u8 [n], nonzero = push right (+10 N), zero = push left;
+ *          NULL = random actions from the action stream of s->seed (with
+ *          s->policy_w set: the MLP policy's actions; CP_RESIDENT only).
+ * obs [4][n], reward [n], done [n]: optional outputs for this step.         */
+int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *reward, uint8_t *done);
+
+/* n_steps consecutive steps from s->t with random actions from the action
+ * stream of `seed` (or the MLP policy when s->policy_w is set), then
+ * s->t += n_steps.  n_steps == 0 is a no-op.  Equivalent, bit for bit, to
+ * n_steps calls of cp_step with the same action source.  traj may be NULL.
+ * CP_UNFUSED and CP_FUSED launch one step at a time; CP_RESIDENT launches a
+ * single kernel for the whole rollout.                                      */
+int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
+
+/* Bytes of workspace CP_UNFUSED needs for n environments (0 for the other
+ * variants, or for n out of range).                                         */
+size_t cp_workspace_bytes(int64_t n, int32_t variant);
+
+/* Message of the last failing call on this thread ("" if none).            */
+const char *cp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* CARTPOLE_H */

@@ -176,15 +176,19 @@ def rollout(st: OracleState, T, act_seed=None, actions=None, policy_w=None, traj
     actions: uint8 [T, m] explicit actions (optional);
     policy_w: uint16 [4480] bf16 MLP weights (optional);
     otherwise random actions from ``act_seed`` (default: the state's seed).
-    traj=True also returns obs [T,4,m], reward [T,m], done [T,m].
+    traj=True also returns obs [T,4,m], reward [T,m], done [T,m]; a tuple of
+    names (e.g. ("done",)) returns only those.
     """
     m, T = st.m, int(T)
     act_seed = st.seed if act_seed is None else int(act_seed)
     out = {"done_count": np.zeros(m, np.uint32), "total_reward": np.zeros(m, np.float32),
            "ret_sum": np.zeros(m, np.uint32)}
-    if traj:
+    want = ("obs", "reward", "done") if traj is True else tuple(traj or ())
+    if "obs" in want:
         out["obs"] = np.zeros((T, 4, m), np.float32)
+    if "reward" in want:
         out["reward"] = np.zeros((T, m), np.float32)
+    if "done" in want:
         out["done"] = np.zeros((T, m), np.uint8)
     if actions is not None:
         actions = np.ascontiguousarray(actions, np.uint8)

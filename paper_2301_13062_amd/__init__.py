@@ -1,0 +1,167 @@
+"""Batched cart-pole environment step on AMD Instinct MI355X (gfx950).
+
+A thin ctypes binding over ``libcartpole.so`` (C ABI in ``include/cartpole.h``):
+argument marshalling only, every step runs in the library's HIP kernels.
+PyTorch provides device memory and the HIP stream.  There is no CPU
+fallback: without the built library (or without a GPU) the calls raise.
+
+    import torch, paper_2301_13062_amd as cp
+    s = cp.CartPoleStates(65536, variant=cp.CP_FUSED)
+    cp.cp_init(s, seed=0)
+    cp.cp_rollout(s, 1000, seed=0)
+"""
+import ctypes
+import os
+
+import torch
+
+CP_UNFUSED, CP_FUSED, CP_RESIDENT = 0, 1, 2
+VARIANTS = {"unfused": CP_UNFUSED, "fused": CP_FUSED, "resident": CP_RESIDENT}
+CP_OK, CP_ERR_NULL, CP_ERR_SIZE, CP_ERR_ALIGN, CP_ERR_RANGE, CP_ERR_HIP, CP_ERR_UNSUPPORTED = (
+    0, -1, -2, -3, -4, -5, -6)
+CP_POLICY_WEIGHTS = 4480
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_build", "libcartpole.so")
+
+_p = ctypes.c_void_p
+
+
+class cp_states(ctypes.Structure):
+    _fields_ = [("x", _p), ("x_dot", _p), ("theta", _p), ("theta_dot", _p),
+                ("ep_index", _p), ("ep_len", _p), ("n", ctypes.c_int64),
+                ("env_base", ctypes.c_uint32), ("variant", ctypes.c_int32),
+                ("seed", ctypes.c_uint64), ("t", ctypes.c_uint64), ("stream", _p),
+                ("policy_w", _p), ("workspace", _p), ("workspace_bytes", ctypes.c_size_t)]
+
+
+class cp_traj(ctypes.Structure):
+    _fields_ = [("obs", _p), ("reward", _p), ("done", _p), ("done_count", _p),
+                ("total_reward", _p), ("ret_sum", _p), ("global", _p)]
+
+
+class CartPoleError(RuntimeError):
+    def __init__(self, code, message):
+        super().__init__(f"cartpole error {code}: {message}")
+        self.code = code
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() "
+                              "or python paper_2301_13062_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.cp_init.argtypes = [P(cp_states), ctypes.c_uint64]
+        L.cp_step.argtypes = [P(cp_states), _p, _p, _p, _p]
+        L.cp_rollout.argtypes = [P(cp_states), ctypes.c_int64, ctypes.c_uint64, P(cp_traj)]
+        L.cp_workspace_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32]
+        L.cp_workspace_bytes.restype = ctypes.c_size_t
+        L.cp_last_error.argtypes = []
+        L.cp_last_error.restype = ctypes.c_char_p
+        for f in (L.cp_init, L.cp_step, L.cp_rollout):
+            f.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _check(code):
+    if code != CP_OK:
+        raise CartPoleError(code, lib().cp_last_error().decode())
+
+
+class CartPoleStates:
+    """Device-resident batch state (structure of arrays) plus the handle.
+
+    x, x_dot, theta, theta_dot: float32 [n]; ep_index, ep_len: int32 [n]
+    holding uint32 values.  ``seed`` and ``t`` mirror the handle's counters.
+    """
+
+    def __init__(self, n, variant=CP_FUSED, device="cuda", env_base=0, policy_w=None,
+                 workspace=None):
+        self.n, self.env_base = int(n), int(env_base)
+        self.variant = VARIANTS.get(variant, variant)
+        f32 = dict(dtype=torch.float32, device=device)
+        i32 = dict(dtype=torch.int32, device=device)
+        self.x, self.x_dot = torch.empty(self.n, **f32), torch.empty(self.n, **f32)
+        self.theta, self.theta_dot = torch.empty(self.n, **f32), torch.empty(self.n, **f32)
+        self.ep_index, self.ep_len = torch.zeros(self.n, **i32), torch.zeros(self.n, **i32)
+        self.policy_w = policy_w
+        self.workspace = workspace
+        if self.variant == CP_UNFUSED and workspace is None:
+            nbytes = cp_workspace_bytes(self.n, CP_UNFUSED)
+            self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.seed, self.t = 0, 0
+        self.stream = None  # None = torch's current stream at call time
+
+    def handle(self):
+        st = self.stream if self.stream is not None else torch.cuda.current_stream()
+        h = cp_states(_ptr(self.x), _ptr(self.x_dot), _ptr(self.theta), _ptr(self.theta_dot),
+                      _ptr(self.ep_index), _ptr(self.ep_len), self.n, self.env_base,
+                      self.variant, self.seed, self.t, st.cuda_stream, _ptr(self.policy_w),
+                      _ptr(self.workspace),
+                      0 if self.workspace is None else self.workspace.numel())
+        return h
+
+    def _sync_back(self, h):
+        self.seed, self.t = int(h.seed), int(h.t)
+
+    def state(self):
+        return torch.stack([self.x, self.x_dot, self.theta, self.theta_dot])
+
+
+class Trajectory:
+    """Optional rollout outputs (torch tensors, any may be None)."""
+
+    def __init__(self, n, T, device="cuda", obs=True, reward=True, done=True, stats=True,
+                 totals=True):
+        f32 = dict(dtype=torch.float32, device=device)
+        self.obs = torch.empty((T, 4, n), **f32) if obs else None
+        self.reward = torch.empty((T, n), **f32) if reward else None
+        self.done = torch.empty((T, n), dtype=torch.uint8, device=device) if done else None
+        self.done_count = torch.empty(n, dtype=torch.int32, device=device) if stats else None
+        self.total_reward = torch.empty(n, **f32) if stats else None
+        self.ret_sum = torch.empty(n, dtype=torch.int32, device=device) if stats else None
+        self.totals = torch.zeros(2, dtype=torch.int64, device=device) if totals else None
+
+    def handle(self):
+        return cp_traj(_ptr(self.obs), _ptr(self.reward), _ptr(self.done), _ptr(self.done_count),
+                       _ptr(self.total_reward), _ptr(self.ret_sum), _ptr(self.totals))
+
+
+def cp_init(states: CartPoleStates, seed: int) -> None:
+    h = states.handle()
+    _check(lib().cp_init(ctypes.byref(h), int(seed)))
+    states._sync_back(h)
+
+
+def cp_step(states: CartPoleStates, actions=None, obs=None, reward=None, done=None) -> None:
+    h = states.handle()
+    _check(lib().cp_step(ctypes.byref(h), _ptr(actions), _ptr(obs), _ptr(reward), _ptr(done)))
+    states._sync_back(h)
+
+
+def cp_rollout(states: CartPoleStates, n_steps: int, seed: int, traj: Trajectory = None) -> None:
+    h = states.handle()
+    th = traj.handle() if traj is not None else None
+    _check(lib().cp_rollout(ctypes.byref(h), int(n_steps), int(seed),
+                            ctypes.byref(th) if th is not None else None))
+    states._sync_back(h)
+
+
+def cp_workspace_bytes(n: int, variant: int) -> int:
+    return int(lib().cp_workspace_bytes(int(n), int(variant)))
+
+
+def cp_last_error() -> str:
+    return lib().cp_last_error().decode()

@@ -1,0 +1,205 @@
+// cp_capi.hip -- the C ABI of libcartpole.so (declared in cartpole.h):
+// argument validation (finished before any HIP call), stream-key
+// derivation, fusion-level dispatch and error reporting.
+#include <cstdarg>
+#include <cstdint>
+#include <cstdio>
+
+#include "cartpole.h"
+#include "cp_launch.h"
+
+#define CP_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+thread_local char g_err[512];
+
+int fail(int code, const char *fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return code;
+}
+
+int ok() {
+  g_err[0] = '\0';
+  return CP_OK;
+}
+
+bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0u; }
+
+int check_states(const cp_states *s) {
+  if (!s) return fail(CP_ERR_NULL, "cp_states pointer is NULL");
+  if (!s->x || !s->x_dot || !s->theta || !s->theta_dot || !s->ep_index || !s->ep_len)
+    return fail(CP_ERR_NULL, "a state array (x, x_dot, theta, theta_dot, ep_index, ep_len) is NULL");
+  if (s->n < 1 || s->n > INT32_MAX)
+    return fail(CP_ERR_SIZE, "n = %lld is outside [1, 2^31 - 1]", (long long)s->n);
+  if (uint64_t(s->env_base) + uint64_t(s->n) > (uint64_t(1) << 32))
+    return fail(CP_ERR_RANGE, "env_base + n exceeds 2^32");
+  if (!aligned4(s->x) || !aligned4(s->x_dot) || !aligned4(s->theta) || !aligned4(s->theta_dot) ||
+      !aligned4(s->ep_index) || !aligned4(s->ep_len))
+    return fail(CP_ERR_ALIGN, "state arrays must be 4-byte aligned");
+  if (s->variant != CP_UNFUSED && s->variant != CP_FUSED && s->variant != CP_RESIDENT)
+    return fail(CP_ERR_UNSUPPORTED, "unknown variant %d", (int)s->variant);
+  return CP_OK;
+}
+
+int check_steps(const cp_states *s, uint64_t n_steps) {
+  if (s->t >= CP_MAX_STEPS || n_steps > CP_MAX_STEPS - 1u - s->t)
+    return fail(CP_ERR_RANGE, "step counter t = %llu plus %llu steps must stay below 2^31",
+                (unsigned long long)s->t, (unsigned long long)n_steps);
+  return CP_OK;
+}
+
+int check_workspace(const cp_states *s) {
+  if (s->variant != CP_UNFUSED) return CP_OK;
+  const size_t need = cp::unfused_workspace_bytes(uint32_t(s->n));
+  if (!s->workspace) return fail(CP_ERR_NULL, "CP_UNFUSED needs a workspace of %zu bytes", need);
+  if (!aligned4(s->workspace)) return fail(CP_ERR_ALIGN, "workspace must be 4-byte aligned");
+  if (s->workspace_bytes < need)
+    return fail(CP_ERR_SIZE, "workspace has %zu bytes, CP_UNFUSED needs %zu", s->workspace_bytes,
+                need);
+  return CP_OK;
+}
+
+int hip_status(hipError_t e, const char *what) {
+  if (e != hipSuccess) return fail(CP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+  return CP_OK;
+}
+
+cp::StepParams step_params(const cp_states *s, uint64_t act_seed) {
+  cp::StepParams p{};
+  p.x = s->x;
+  p.xd = s->x_dot;
+  p.th = s->theta;
+  p.thd = s->theta_dot;
+  p.ep_index = s->ep_index;
+  p.ep_len = s->ep_len;
+  p.n = uint32_t(s->n);
+  p.env_base = s->env_base;
+  p.kact = cp::stream_key(act_seed, cp::kTagAction);
+  p.krst = cp::stream_key(s->seed, cp::kTagReset);
+  p.t = uint32_t(s->t);
+  return p;
+}
+
+}  // namespace
+
+CP_API int cp_init(cp_states *s, uint64_t seed) {
+  if (int e = check_states(s)) return e;
+  const cp::U2 krst = cp::stream_key(seed, cp::kTagReset);
+  hipStream_t st = static_cast<hipStream_t>(s->stream);
+  if (int e = hip_status(cp::launch_init(s->x, s->x_dot, s->theta, s->theta_dot, s->ep_index,
+                                         s->ep_len, uint32_t(s->n), s->env_base, krst, st),
+                         "cp_init launch"))
+    return e;
+  s->seed = seed;
+  s->t = 0;
+  return ok();
+}
+
+CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *reward,
+                   uint8_t *done) {
+  if (int e = check_states(s)) return e;
+  if (int e = check_steps(s, 1)) return e;
+  if (int e = check_workspace(s)) return e;
+  if ((obs && !aligned4(obs)) || (reward && !aligned4(reward)))
+    return fail(CP_ERR_ALIGN, "obs and reward must be 4-byte aligned");
+  hipStream_t st = static_cast<hipStream_t>(s->stream);
+  const bool policy = s->policy_w && !actions;
+  if (policy && s->variant != CP_RESIDENT)
+    return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
+  if (policy && !cp::kPolicyBuilt)
+    return fail(CP_ERR_UNSUPPORTED, "the MLP policy kernel is not part of this build");
+
+  hipError_t err;
+  if (s->variant == CP_RESIDENT && !actions) {
+    // One step of the resident kernel, its trajectory outputs being this
+    // step's outputs ([1][4][n] == [4][n]).
+    cp::StepParams sp = step_params(s, s->seed);
+    cp::RolloutParams p{};
+    p.x = sp.x; p.xd = sp.xd; p.th = sp.th; p.thd = sp.thd;
+    p.ep_index = sp.ep_index; p.ep_len = sp.ep_len;
+    p.n = sp.n; p.env_base = sp.env_base; p.kact = sp.kact; p.krst = sp.krst;
+    p.t0 = sp.t; p.T = 1u;
+    p.policy_w = policy ? s->policy_w : nullptr;
+    p.obs = obs; p.reward = reward; p.done = done;
+    err = cp::launch_resident(p, st);
+  } else {
+    cp::StepParams p = step_params(s, s->seed);
+    p.actions = actions;
+    p.obs = obs;
+    p.reward = reward;
+    p.done = done;
+    // Explicit actions under CP_RESIDENT: a single step is the fused step.
+    err = (s->variant == CP_UNFUSED) ? cp::launch_unfused_step(p, s->workspace, st)
+                                     : cp::launch_fused_step(p, st);
+  }
+  if (int e = hip_status(err, "cp_step launch")) return e;
+  s->t += 1;
+  return ok();
+}
+
+CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj) {
+  if (int e = check_states(s)) return e;
+  if (n_steps < 0) return fail(CP_ERR_SIZE, "n_steps = %lld is negative", (long long)n_steps);
+  if (int e = check_steps(s, uint64_t(n_steps))) return e;
+  if (int e = check_workspace(s)) return e;
+  cp_traj none{};
+  const cp_traj &tr = traj ? *traj : none;
+  if ((tr.obs && !aligned4(tr.obs)) || (tr.reward && !aligned4(tr.reward)) ||
+      (tr.done_count && !aligned4(tr.done_count)) ||
+      (tr.total_reward && !aligned4(tr.total_reward)) || (tr.ret_sum && !aligned4(tr.ret_sum)) ||
+      (tr.global && (reinterpret_cast<uintptr_t>(tr.global) & 7u)))
+    return fail(CP_ERR_ALIGN, "trajectory outputs must be 4-byte aligned (global: 8-byte)");
+  if (s->policy_w && s->variant != CP_RESIDENT)
+    return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
+  if (s->policy_w && !cp::kPolicyBuilt)
+    return fail(CP_ERR_UNSUPPORTED, "the MLP policy kernel is not part of this build");
+  if (n_steps == 0) return ok();
+
+  hipStream_t st = static_cast<hipStream_t>(s->stream);
+  const size_t n = size_t(s->n);
+  if (s->variant == CP_RESIDENT) {
+    cp::StepParams sp = step_params(s, seed);
+    cp::RolloutParams p{};
+    p.x = sp.x; p.xd = sp.xd; p.th = sp.th; p.thd = sp.thd;
+    p.ep_index = sp.ep_index; p.ep_len = sp.ep_len;
+    p.n = sp.n; p.env_base = sp.env_base; p.kact = sp.kact; p.krst = sp.krst;
+    p.t0 = sp.t; p.T = uint32_t(n_steps);
+    p.policy_w = s->policy_w;
+    p.obs = tr.obs; p.reward = tr.reward; p.done = tr.done;
+    p.done_count = tr.done_count; p.total_reward = tr.total_reward; p.ret_sum = tr.ret_sum;
+    p.global = tr.global;
+    if (int e = hip_status(cp::launch_resident(p, st), "cp_rollout launch")) return e;
+  } else {
+    cp::StepParams p = step_params(s, seed);
+    p.done_count = tr.done_count;
+    p.total_reward = tr.total_reward;
+    p.ret_sum = tr.ret_sum;
+    p.global = tr.global;
+    for (int64_t j = 0; j < n_steps; ++j) {
+      p.t = uint32_t(s->t + uint64_t(j));
+      p.first = j == 0;
+      p.obs = tr.obs ? tr.obs + size_t(j) * 4u * n : nullptr;
+      p.reward = tr.reward ? tr.reward + size_t(j) * n : nullptr;
+      p.done = tr.done ? tr.done + size_t(j) * n : nullptr;
+      hipError_t err = (s->variant == CP_UNFUSED) ? cp::launch_unfused_step(p, s->workspace, st)
+                                                  : cp::launch_fused_step(p, st);
+      if (int e = hip_status(err, "cp_rollout launch")) {
+        s->t += uint64_t(j);  // steps already queued stay counted
+        return e;
+      }
+    }
+  }
+  s->t += uint64_t(n_steps);
+  return ok();
+}
+
+CP_API size_t cp_workspace_bytes(int64_t n, int32_t variant) {
+  if (variant != CP_UNFUSED || n < 1 || n > INT32_MAX) return 0;
+  return cp::unfused_workspace_bytes(uint32_t(n));
+}
+
+CP_API const char *cp_last_error(void) { return g_err; }

@@ -1,0 +1,175 @@
+// cp_device.h -- device-side building blocks of the batched cart-pole step
+// for gfx950: the counter-based generator, the dynamics of one step, the
+// termination test and the reset draw.  Every fusion level (per-op chain,
+// fused step, register-resident rollout) is built from these functions, so
+// the levels round identically.
+//
+// Arithmetic contract (shared by all kernels; compiled with
+// -ffp-contract=off): binary32, every operation of the step rounded in the
+// order written below, division correctly rounded.  sin and cos are
+// polynomials on |theta| <= 1/4 (the only angles a non-terminated state can
+// hold) and the library routines beyond.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace cp {
+
+// ---------------------------------------------------------------- constants
+// Classic frictionless cart-pole (the environment of the paper's case study,
+// Sec. "Case Study on Cart-pole"), single precision.
+constexpr float kGravity = 9.8f;
+constexpr float kMassCart = 1.0f;
+constexpr float kMassPole = 0.1f;
+constexpr float kTotalMass = kMassPole + kMassCart;          // 1.1f
+constexpr float kHalfLength = 0.5f;
+constexpr float kPoleMassLength = kMassPole * kHalfLength;   // 0.05f
+constexpr float kFourThirds = 4.0f / 3.0f;
+constexpr float kForceMag = 10.0f;
+constexpr float kTau = 0.02f;
+constexpr float kXLimit = 2.4f;
+// 12 degrees in radians, rounded once to binary32 (0x3E567750).
+constexpr float kThetaLimit = 0.209439510239319549f;
+// Reset draws: centred 24-bit integer times 0.1 * 2^-24 (exact power-of-two
+// scaling of 0.1f).
+constexpr float kResetScale = 0x1.99999ap-28f;
+
+constexpr uint32_t kTagAction = 1u;
+constexpr uint32_t kTagReset = 2u;
+
+// ---------------------------------------------------------------- Threefry
+// Threefry-2x32 with 20 rounds (Salmon, Moraes, Dror, Shaw, SC'11): four
+// rounds of add / rotate / xor between key injections; key schedule
+// (k0, k1, k0 ^ k1 ^ 0x1BD11BDA); injection s adds ks[s%3], ks[(s+1)%3] + s.
+__host__ __device__ __forceinline__ uint32_t rotl(uint32_t v, int r) {
+  return (v << r) | (v >> (32 - r));
+}
+
+struct U2 {
+  uint32_t a, b;
+};
+
+#define CP_TF_ROUND(r)  \
+  x0 += x1;             \
+  x1 = rotl(x1, r);     \
+  x1 ^= x0;
+
+__host__ __device__ __forceinline__ U2 threefry2x32(uint32_t k0, uint32_t k1, uint32_t c0,
+                                                   uint32_t c1) {
+  const uint32_t k2 = k0 ^ k1 ^ 0x1BD11BDAu;
+  uint32_t x0 = c0 + k0, x1 = c1 + k1;
+  CP_TF_ROUND(13) CP_TF_ROUND(15) CP_TF_ROUND(26) CP_TF_ROUND(6)
+  x0 += k1; x1 += k2 + 1u;
+  CP_TF_ROUND(17) CP_TF_ROUND(29) CP_TF_ROUND(16) CP_TF_ROUND(24)
+  x0 += k2; x1 += k0 + 2u;
+  CP_TF_ROUND(13) CP_TF_ROUND(15) CP_TF_ROUND(26) CP_TF_ROUND(6)
+  x0 += k0; x1 += k1 + 3u;
+  CP_TF_ROUND(17) CP_TF_ROUND(29) CP_TF_ROUND(16) CP_TF_ROUND(24)
+  x0 += k1; x1 += k2 + 4u;
+  CP_TF_ROUND(13) CP_TF_ROUND(15) CP_TF_ROUND(26) CP_TF_ROUND(6)
+  x0 += k2; x1 += k0 + 5u;
+  return U2{x0, x1};
+}
+#undef CP_TF_ROUND
+
+// Key of a random stream: the generator keyed by (seed_hi, seed_lo) on
+// counter (tag, 0).  Computed once per call on the host.
+__host__ __device__ __forceinline__ U2 stream_key(uint64_t seed, uint32_t tag) {
+  return threefry2x32(uint32_t(seed >> 32), uint32_t(seed), tag, 0u);
+}
+
+// Random action bit of step t: bit (t mod 64) of the block drawn on counter
+// (env, t / 64); bits 0..31 from the first word, 32..63 from the second.
+__device__ __forceinline__ uint32_t action_from_block(U2 w, uint32_t t) {
+  const uint32_t word = (t & 32u) ? w.b : w.a;
+  return (word >> (t & 31u)) & 1u;
+}
+
+__device__ __forceinline__ uint32_t action_bit(U2 key, uint32_t env, uint32_t t) {
+  return action_from_block(threefry2x32(key.a, key.b, env, t >> 6), t);
+}
+
+__device__ __forceinline__ float reset_value(uint32_t u) {
+  return float(int32_t(u >> 8) - int32_t(1 << 23)) * kResetScale;
+}
+
+struct State {
+  float x, xd, th, thd;
+};
+
+// Start state of episode k: words from counters (env, 2k) and (env, 2k+1).
+__device__ __forceinline__ State reset_draw(U2 key, uint32_t env, uint32_t k) {
+  const U2 p = threefry2x32(key.a, key.b, env, 2u * k);
+  const U2 q = threefry2x32(key.a, key.b, env, 2u * k + 1u);
+  return State{reset_value(p.a), reset_value(p.b), reset_value(q.a), reset_value(q.b)};
+}
+
+// ---------------------------------------------------------------- sin / cos
+// Taylor polynomials on |th| <= 1/4: the first omitted terms are below
+// 2^-34 relative, so the result is within about half an ulp plus the
+// rounding of the evaluation.
+__device__ __forceinline__ float sin_small(float th) {
+  const float z = th * th;
+  float p = 2.75573192e-06f;                 //  1/9!
+  p = __builtin_fmaf(p, z, -1.98412698e-04f);  // -1/7!
+  p = __builtin_fmaf(p, z, 8.33333333e-03f);   //  1/5!
+  p = __builtin_fmaf(p, z, -1.66666667e-01f);  // -1/3!
+  return __builtin_fmaf(th * z, p, th);
+}
+
+__device__ __forceinline__ float cos_small(float th) {
+  const float z = th * th;
+  float p = 2.48015873e-05f;                   //  1/8!
+  p = __builtin_fmaf(p, z, -1.38888889e-03f);  // -1/6!
+  p = __builtin_fmaf(p, z, 4.16666667e-02f);   //  1/4!
+  p = __builtin_fmaf(p, z, -0.5f);             // -1/2!
+  return __builtin_fmaf(z, p, 1.0f);
+}
+
+__device__ __forceinline__ float sin_th(float th) {
+  return (__builtin_fabsf(th) <= 0.25f) ? sin_small(th) : sinf(th);
+}
+
+__device__ __forceinline__ float cos_th(float th) {
+  return (__builtin_fabsf(th) <= 0.25f) ? cos_small(th) : cosf(th);
+}
+
+// ---------------------------------------------------------------- dynamics
+// One explicit-Euler step of the cart-pole equations of motion (right-hand
+// sides use the old state), binary32, in this operation order:
+//   temp  = (F + (pml * thd^2) * sin) / M
+//   thacc = (g sin - cos temp) / (l (4/3 - (mp cos^2) / M))
+//   xacc  = temp - ((pml * thacc) * cos) / M
+__device__ __forceinline__ float force_of(uint32_t a) { return a ? kForceMag : -kForceMag; }
+
+__device__ __forceinline__ State dynamics(State s, float force) {
+  const float c = cos_th(s.th);
+  const float sn = sin_th(s.th);
+  const float thd2 = s.thd * s.thd;
+  const float c2 = c * c;
+  const float temp = (force + kPoleMassLength * thd2 * sn) / kTotalMass;
+  const float thacc =
+      (kGravity * sn - c * temp) / (kHalfLength * (kFourThirds - kMassPole * c2 / kTotalMass));
+  const float xacc = temp - kPoleMassLength * thacc * c / kTotalMass;
+  State o;
+  o.x = s.x + kTau * s.xd;
+  o.xd = s.xd + kTau * xacc;
+  o.th = s.th + kTau * s.thd;
+  o.thd = s.thd + kTau * thacc;
+  return o;
+}
+
+// Strict limits on the post-update state.
+__device__ __forceinline__ bool terminated(State s) {
+  return s.x < -kXLimit || s.x > kXLimit || s.th < -kThetaLimit || s.th > kThetaLimit;
+}
+
+// ---------------------------------------------------------------- wave helpers
+__device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+  return v;
+}
+
+}  // namespace cp

@@ -1,0 +1,60 @@
+// cp_launch.h -- parameter blocks and launchers shared by the kernel files
+// and the C-ABI layer.  Internal to libcartpole.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "cp_device.h"
+
+namespace cp {
+
+// Batch state and the per-step outputs of one step (fused or unfused).
+struct StepParams {
+  float *x, *xd, *th, *thd;
+  uint32_t *ep_index, *ep_len;
+  uint32_t n, env_base;
+  const uint8_t *actions;  // explicit actions [n] or nullptr (random stream)
+  U2 kact, krst;           // stream keys (action, reset)
+  uint32_t t;              // global step index of this step
+  float *obs;              // [4][n] or nullptr
+  float *reward;           // [n] or nullptr
+  uint8_t *done;           // [n] or nullptr
+  uint32_t *done_count;    // [n] rollout accumulators, or nullptr
+  float *total_reward;
+  uint32_t *ret_sum;
+  uint32_t first;          // 1: accumulators start from zero at this step
+  unsigned long long *global;  // [2] or nullptr
+};
+
+// A whole rollout of T steps in one launch (register-resident).
+struct RolloutParams {
+  float *x, *xd, *th, *thd;
+  uint32_t *ep_index, *ep_len;
+  uint32_t n, env_base;
+  U2 kact, krst;
+  uint32_t t0, T;
+  const uint16_t *policy_w;  // bf16 MLP weights or nullptr
+  float *obs;                // [T][4][n] or nullptr
+  float *reward;             // [T][n]
+  uint8_t *done;             // [T][n]
+  uint32_t *done_count;      // [n]
+  float *total_reward;       // [n]
+  uint32_t *ret_sum;         // [n]
+  unsigned long long *global;
+};
+
+hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_index,
+                       uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst,
+                       hipStream_t stream);
+hipError_t launch_fused_step(const StepParams &p, hipStream_t stream);
+hipError_t launch_resident(const RolloutParams &p, hipStream_t stream);
+constexpr bool kPolicyBuilt = false;
+
+// Unfused level: one kernel per primitive operation; temporaries live in the
+// caller's workspace.
+size_t unfused_workspace_bytes(uint32_t n);
+hipError_t launch_unfused_step(const StepParams &p, void *workspace, hipStream_t stream);
+
+}  // namespace cp

@@ -20,3 +20,13 @@ def gpu():
     if not torch.cuda.is_available():
         pytest.fail("GPU test selected but no HIP device is visible")
     return torch.device("cuda:0")
+
+
+@pytest.fixture(autouse=True)
+def _announce_gpu_case(request):
+    """Name each GPU case on the real stderr before it touches the device,
+    so a run that dies mid-test still says which case it was."""
+    if request.node.get_closest_marker("gpu") is not None:
+        sys.__stderr__.write(f"\n[gpu-case] {request.node.nodeid}\n")
+        sys.__stderr__.flush()
+    yield

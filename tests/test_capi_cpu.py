@@ -1,0 +1,135 @@
+"""The C-ABI library without a GPU: it loads, exports every declared entry
+point, and rejects bad arguments before any HIP call (nothing here launches
+a kernel; every call is built to fail validation or to be a no-op)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+import paper_2301_13062_amd as cp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "cartpole.h")
+
+# Fake, never-dereferenced device addresses: aligned and misaligned.
+A = 0x7F0000000000
+MIS = A + 2
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(cp_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert {"cp_init", "cp_step", "cp_rollout", "cp_workspace_bytes", "cp_last_error"} <= set(names)
+    L = cp.lib()
+    for n in names:
+        assert hasattr(L, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", cp.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = sorted(set(re.findall(r"\bT (cp_\w+)", out)))
+    assert exported == names  # nothing undeclared leaks out
+
+
+def handle(**kw):
+    h = cp.cp_states(A, A + 0x1000, A + 0x2000, A + 0x3000, A + 0x4000, A + 0x5000, 1000, 0,
+                     cp.CP_FUSED, 123, 7, None, None, None, 0)
+    for k, v in kw.items():
+        setattr(h, k, v)
+    return h
+
+
+def call_init(h):
+    return cp.lib().cp_init(ctypes.byref(h), 5)
+
+
+def call_step(h, actions=None, obs=None):
+    return cp.lib().cp_step(ctypes.byref(h), actions, obs, None, None)
+
+
+def call_rollout(h, n, traj=None):
+    return cp.lib().cp_rollout(ctypes.byref(h), n, 0, ctypes.byref(traj) if traj else None)
+
+
+@pytest.mark.parametrize("fn", [call_init, call_step, lambda h: call_rollout(h, 3)])
+@pytest.mark.parametrize("field,value,code", [
+    ("x", None, cp.CP_ERR_NULL),
+    ("ep_len", None, cp.CP_ERR_NULL),
+    ("n", 0, cp.CP_ERR_SIZE),
+    ("n", -5, cp.CP_ERR_SIZE),
+    ("n", 2 ** 31, cp.CP_ERR_SIZE),
+    ("theta", MIS, cp.CP_ERR_ALIGN),
+    ("ep_index", A + 1, cp.CP_ERR_ALIGN),
+    ("env_base", 2 ** 32 - 10, cp.CP_ERR_RANGE),
+    ("variant", 3, cp.CP_ERR_UNSUPPORTED),
+    ("variant", -1, cp.CP_ERR_UNSUPPORTED),
+])
+def test_rejects_bad_state(fn, field, value, code):
+    h = handle(**{field: value})
+    assert fn(h) == code
+    assert cp.lib().cp_last_error().decode() != ""
+    assert h.t == 7 and h.seed == 123  # untouched
+
+
+def test_null_handle():
+    L = cp.lib()
+    assert L.cp_init(None, 0) == cp.CP_ERR_NULL
+    assert L.cp_step(None, None, None, None, None) == cp.CP_ERR_NULL
+    assert L.cp_rollout(None, 1, 0, None) == cp.CP_ERR_NULL
+
+
+def test_step_counter_range():
+    assert call_step(handle(t=2 ** 31 - 1)) == cp.CP_ERR_RANGE
+    assert call_rollout(handle(t=2 ** 31 - 10), 10) == cp.CP_ERR_RANGE
+    assert call_rollout(handle(t=0), 2 ** 31) == cp.CP_ERR_RANGE
+    assert call_rollout(handle(), -1) == cp.CP_ERR_SIZE
+
+
+def test_rollout_zero_steps_is_a_noop():
+    h = handle()
+    assert call_rollout(h, 0) == cp.CP_OK
+    assert h.t == 7 and cp.lib().cp_last_error().decode() == ""
+
+
+def test_output_alignment():
+    assert call_step(handle(), obs=MIS) == cp.CP_ERR_ALIGN
+    tr = cp.cp_traj(None, A + 2, None, None, None, None, None)
+    assert call_rollout(handle(), 4, tr) == cp.CP_ERR_ALIGN
+    tr = cp.cp_traj(None, None, None, None, None, None, A + 4)  # u64 totals need 8 bytes
+    assert call_rollout(handle(), 4, tr) == cp.CP_ERR_ALIGN
+
+
+def test_unfused_workspace_checks():
+    need = cp.cp_workspace_bytes(1000, cp.CP_UNFUSED)
+    assert need >= 1000 * 4 * 30
+    assert cp.cp_workspace_bytes(1000, cp.CP_FUSED) == 0
+    assert cp.cp_workspace_bytes(0, cp.CP_UNFUSED) == 0
+    assert call_step(handle(variant=cp.CP_UNFUSED)) == cp.CP_ERR_NULL
+    h = handle(variant=cp.CP_UNFUSED, workspace=A, workspace_bytes=need - 1)
+    assert call_step(h) == cp.CP_ERR_SIZE
+    assert call_rollout(h, 2) == cp.CP_ERR_SIZE
+
+
+def test_policy_needs_resident_variant():
+    for v in (cp.CP_FUSED, cp.CP_UNFUSED):
+        h = handle(variant=v, policy_w=A, workspace=A,
+                   workspace_bytes=cp.cp_workspace_bytes(1000, cp.CP_UNFUSED))
+        assert call_step(h) == cp.CP_ERR_UNSUPPORTED
+        assert call_rollout(h, 1) == cp.CP_ERR_UNSUPPORTED
+
+
+def test_product_path_does_not_touch_the_oracle():
+    # The library and the binding never reference the oracle.
+    pkg = os.path.join(ROOT, "paper_2301_13062_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".h", ".cpp")):
+                text = open(os.path.join(dirpath, f)).read()
+                assert "oracle" not in text.lower(), f
+    out = subprocess.run(["nm", "-D", cp.LIB_PATH], capture_output=True, text=True).stdout
+    assert "orc_" not in out
