@@ -1,0 +1,246 @@
+"""Benchmark of the batched cart-pole step on one MI355X.
+
+Headline (the JSON line's `value`): 65,536 environments advanced one step
+per kernel launch by the fused step kernel, random actions, each step
+writing obs / reward / done -- the configuration on which the paper's
+fusion comparison is made (unfused per-op chain vs one fused kernel).  A
+"step" of this benchmark is one such launch over the whole batch.
+
+Also measured in the same run (extra keys of the same JSON line):
+  unfused   the same workload through the one-op-per-kernel chain;
+  configs   1,024 x 200 and 1,048,576 x 1,000 register-resident rollouts,
+            16,777,216 x 100 streaming fused steps with full trajectory;
+  roofline  HBM roofline of the fused step kernel: algorithmic bytes per
+            launch over the mean launch duration (HIP events around the
+            timed region of back-to-back launches, divided by the launches);
+  cpu_baseline  the CPU oracle on the host cores (one thread).
+
+Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
+FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector (packed), TFLOP/s
+METRIC = "env-steps/sec on 1 MI355X; achieved HBM GB/s (or VALU %) vs peak"
+
+# Algorithmic HBM bytes per environment-step of the fused step kernel:
+# reads x, x_dot, theta, theta_dot, ep_len (20 B); writes the same (20 B)
+# plus obs (16 B), reward (4 B) and done (1 B).  The episode index is read
+# and written only on termination (about 4.5% of steps) and is not counted.
+STEP_BYTES_WITH_OUTPUTS = 61
+# Same kernel without per-step outputs (state round trip only).
+STEP_BYTES_STATE_ONLY = 40
+# Algorithmic binary32 operations per environment-step of the dynamics
+# (sin, cos, 2 squares, 15 mul/add/sub/div in the accelerations, 8 in the
+# Euler update, 4 comparisons).
+STEP_FLOPS = 31
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--quick", action="store_true", help="headline only, no extra configs")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--only", choices=["resident_1024x200", "resident_1048576x1000",
+                                       "streaming_16777216x100", "copy"],
+                    help="run one workload only (for counter collection); prints its JSON")
+    return ap.parse_args()
+
+
+def _sync():
+    import torch
+
+    torch.cuda.synchronize()
+
+
+def timed(fn, reps=1):
+    """Wall time and HIP-event time (ms) of reps calls of fn()."""
+    import torch
+
+    _sync()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record()
+    for _ in range(reps):
+        fn()
+    e1.record()
+    _sync()
+    return (time.perf_counter() - t0) * 1e3, e0.elapsed_time(e1)
+
+
+def bench_headline(cp, K, W):
+    import torch
+
+    n = 65536
+    out = {}
+    for name, variant in (("fused", cp.CP_FUSED), ("unfused", cp.CP_UNFUSED)):
+        s = cp.CartPoleStates(n, variant=variant)
+        cp.cp_init(s, 0)
+        warm = cp.Trajectory(n, W, stats=False, totals=False)
+        cp.cp_rollout(s, W, 0, warm)
+        del warm
+        tr = cp.Trajectory(n, K, stats=False, totals=False)
+        # the library launches the K step kernels back to back on torch's
+        # current stream; HIP events bracket the whole timed region
+        wall, ev = timed(lambda: cp.cp_rollout(s, K, 0, tr))
+        out[name] = {"wall_ms": wall, "event_ms": ev, "env_steps_per_s": n * K / (wall * 1e-3),
+                     "us_per_step": wall * 1e3 / K, "event_us_per_step": ev * 1e3 / K}
+        del tr
+    return n, out
+
+
+def bench_copy():
+    """A plain 1 GiB copy-like elementwise kernel (reads 1 GiB, writes 1 GiB):
+    the reference for scaling HBM byte counters."""
+    import torch
+
+    src = torch.ones(1 << 28, device="cuda")
+    dst = torch.empty_like(src)
+    torch.mul(src, 1.0, out=dst)
+    wall, ev = timed(lambda: torch.mul(src, 1.0, out=dst), reps=5)
+    return {"bytes_read": 1 << 30, "bytes_written": 1 << 30, "ms": ev / 5,
+            "GB_per_s": 2 * (1 << 30) / (ev / 5 * 1e-3) / 1e9}
+
+
+def bench_configs(cp, only=None):
+    import torch
+
+    res = {}
+    want = (lambda k: only is None or only == k)
+    if want("resident_1024x200"):
+        res["resident_1024x200"] = _resident_small(cp)
+    if want("resident_1048576x1000"):
+        res["resident_1048576x1000"] = _resident_large(cp)
+    if want("streaming_16777216x100"):
+        res["streaming_16777216x100"] = _streaming(cp)
+    torch.cuda.empty_cache()
+    return res
+
+
+def _resident_small(cp):
+    # 1,024 x 200, register-resident (latency-bound: 16 waves)
+    n, T = 1024, 200
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    cp.cp_init(s, 0)
+    tr = cp.Trajectory(n, T, obs=False, reward=False, done=False)
+    cp.cp_rollout(s, T, 0, tr)
+    wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=20)
+    return {"env_steps_per_s": n * T * 20 / (ev * 1e-3), "ms": ev / 20}
+
+
+def _resident_large(cp):
+    # 1,048,576 x 1,000, register-resident, final state + per-env stats
+    n, T = 1 << 20, 1000
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    cp.cp_init(s, 0)
+    tr = cp.Trajectory(n, T, obs=False, reward=False, done=False)
+    cp.cp_rollout(s, T, 0, tr)
+    wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=5)
+    mean_ms = ev / 5
+    eps = n * T / (mean_ms * 1e-3)
+    return {"env_steps_per_s": eps, "ms": mean_ms,
+            "roofline": {"bound": "alu", "achieved": eps * STEP_FLOPS / 1e12,
+                         "peak": FP32_VALU_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": eps * STEP_FLOPS / 1e12 / FP32_VALU_PEAK_TFLOPS}}
+
+
+def _streaming(cp):
+    import torch
+
+    # 16,777,216 x 100, fused step per launch with full trajectory (HBM-bound)
+    n, T = 1 << 24, 100
+    s = cp.CartPoleStates(n, variant=cp.CP_FUSED)
+    cp.cp_init(s, 0)
+    tr = cp.Trajectory(n, T, stats=False, totals=False)
+    cp.cp_rollout(s, T, 0, tr)
+    wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=3)
+    mean_ms = ev / (3 * T)  # per launch: T back-to-back step kernels per rollout
+    gbs = STEP_BYTES_WITH_OUTPUTS * n / (mean_ms * 1e-3) / 1e9
+    out = {"env_steps_per_s": n * T * 3 / (ev * 1e-3), "ms": ev / 3,
+           "kernel_mean_us": mean_ms * 1e3,
+           "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": STEP_BYTES_WITH_OUTPUTS}}
+    del s, tr
+    torch.cuda.empty_cache()
+    return out
+
+
+def cpu_baseline():
+    import oracle as O
+
+    n, T = 65536, 1000
+    o = O.OracleState(n)
+    O.init(o, 0)
+    t0 = time.perf_counter()
+    O.rollout(o, T, traj=("done",))
+    dt = time.perf_counter() - t0
+    return {"value": n * T / dt, "unit": "env-steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"the whole headline workload ({n} envs x {T} steps, random actions, "
+                      f"done flags kept) on one host thread, {dt:.1f} s"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the batch shards by "
+              "environment index without communication, so a multi-GPU figure is not measured "
+              "here.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import paper_2301_13062_amd as cp
+
+    cp.lib()  # fails loudly without the built library
+    assert torch.cuda.is_available(), "no HIP device"
+    K, W = args.steps, args.warmup
+    if args.only:
+        res = bench_copy() if args.only == "copy" else bench_configs(cp, args.only)[args.only]
+        print(json.dumps({"only": args.only, **res}))
+        return
+
+    n, head = bench_headline(cp, K, W)
+    fused = head["fused"]
+    kern_us = fused["event_us_per_step"]
+    gbs = STEP_BYTES_WITH_OUTPUTS * n / (kern_us * 1e-6) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": fused["env_steps_per_s"],
+        "unit": "env-steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": fused["wall_ms"] / K,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "cart-pole fused step kernel, 65,536 envs, 1 step per launch, "
+                               "random actions, obs/reward/done written every step",
+                   "envs": n, "steps_per_launch": 1, "variant": "fused"},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "bytes_per_env_step": STEP_BYTES_WITH_OUTPUTS,
+                     "kernel_mean_us": kern_us},
+        "unfused": {"env_steps_per_s": head["unfused"]["env_steps_per_s"],
+                    "us_per_step": head["unfused"]["us_per_step"]},
+        "fusion_speedup": fused["env_steps_per_s"] / head["unfused"]["env_steps_per_s"],
+    }
+    if not args.quick:
+        line["configs"] = bench_configs(cp)
+    if not args.no_cpu:
+        line["cpu_baseline"] = cpu_baseline()
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()

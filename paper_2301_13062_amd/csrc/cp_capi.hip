@@ -178,7 +178,11 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
     p.done_count = tr.done_count;
     p.total_reward = tr.total_reward;
     p.ret_sum = tr.ret_sum;
-    p.global = tr.global;
+    if (tr.global)
+      if (int e = hip_status(cp::launch_episode_sums(s->ep_index, s->ep_len, p.n, false, 0u,
+                                                     tr.global, st),
+                             "cp_rollout totals"))
+        return e;
     for (int64_t j = 0; j < n_steps; ++j) {
       p.t = uint32_t(s->t + uint64_t(j));
       p.first = j == 0;
@@ -192,6 +196,14 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
         return e;
       }
     }
+    if (tr.global)
+      if (int e = hip_status(cp::launch_episode_sums(s->ep_index, s->ep_len, p.n, true,
+                                                     uint64_t(n) * uint64_t(n_steps), tr.global,
+                                                     st),
+                             "cp_rollout totals")) {
+        s->t += uint64_t(n_steps);
+        return e;
+      }
   }
   s->t += uint64_t(n_steps);
   return ok();

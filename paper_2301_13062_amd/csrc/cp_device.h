@@ -6,9 +6,10 @@
 //
 // Arithmetic contract (shared by all kernels; compiled with
 // -ffp-contract=off): binary32, every operation of the step rounded in the
-// order written below, division correctly rounded.  sin and cos are
-// polynomials on |theta| <= 1/4 (the only angles a non-terminated state can
-// hold) and the library routines beyond.
+// order written below; divisions are reciprocal products corrected to the
+// rounded quotient (see div_mass, div_rn).  sin and cos are polynomials on
+// |theta| <= 1/4 (the only angles a non-terminated state can hold) and the
+// library routines beyond.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -135,6 +136,46 @@ __device__ __forceinline__ float cos_th(float th) {
   return (__builtin_fabsf(th) <= 0.25f) ? cos_small(th) : cosf(th);
 }
 
+// Both at once; when every lane of the wave holds a small angle (always, for
+// states the library produces) a single uniform branch selects the
+// polynomials.  Per lane the result equals sin_th / cos_th.
+__device__ __forceinline__ void sincos_th(float th, float &sn, float &c) {
+  if (__all(__builtin_fabsf(th) <= 0.25f)) {
+    sn = sin_small(th);
+    c = cos_small(th);
+  } else {
+    sn = sin_th(th);
+    c = cos_th(th);
+  }
+}
+
+// ---------------------------------------------------------------- division
+// Division by the total mass M = 1.1f: the product with the rounded
+// reciprocal, corrected once with the exact residual (Markstein).  Checked
+// against correctly rounded division for every finite binary32 dividend:
+// identical whenever |x| >= 2^-104; below that (where the quotient itself is
+// under 2^-104) the two may differ in the last place.
+constexpr float kInvTotalMass = 1.0f / kTotalMass;
+
+__device__ __forceinline__ float div_mass(float x) {
+  const float q = x * kInvTotalMass;
+  const float r = __builtin_fmaf(-q, kTotalMass, x);
+  return __builtin_fmaf(r, kInvTotalMass, q);
+}
+
+// General division a / b: hardware reciprocal refined by one Newton step to
+// the rounded reciprocal, then the quotient corrected once with the exact
+// residual (Markstein's correction).  Used for the angular acceleration,
+// whose divisor lies in [0.62, 0.67].
+__device__ __forceinline__ float div_rn(float a, float b) {
+  const float y0 = __builtin_amdgcn_rcpf(b);
+  const float e = __builtin_fmaf(-b, y0, 1.0f);
+  const float y = __builtin_fmaf(e, y0, y0);
+  const float q = a * y;
+  const float r = __builtin_fmaf(-q, b, a);
+  return __builtin_fmaf(r, y, q);
+}
+
 // ---------------------------------------------------------------- dynamics
 // One explicit-Euler step of the cart-pole equations of motion (right-hand
 // sides use the old state), binary32, in this operation order:
@@ -144,14 +185,14 @@ __device__ __forceinline__ float cos_th(float th) {
 __device__ __forceinline__ float force_of(uint32_t a) { return a ? kForceMag : -kForceMag; }
 
 __device__ __forceinline__ State dynamics(State s, float force) {
-  const float c = cos_th(s.th);
-  const float sn = sin_th(s.th);
+  float sn, c;
+  sincos_th(s.th, sn, c);
   const float thd2 = s.thd * s.thd;
   const float c2 = c * c;
-  const float temp = (force + kPoleMassLength * thd2 * sn) / kTotalMass;
+  const float temp = div_mass(force + kPoleMassLength * thd2 * sn);
   const float thacc =
-      (kGravity * sn - c * temp) / (kHalfLength * (kFourThirds - kMassPole * c2 / kTotalMass));
-  const float xacc = temp - kPoleMassLength * thacc * c / kTotalMass;
+      div_rn(kGravity * sn - c * temp, kHalfLength * (kFourThirds - div_mass(kMassPole * c2)));
+  const float xacc = temp - div_mass(kPoleMassLength * thacc * c);
   State o;
   o.x = s.x + kTau * s.xd;
   o.xd = s.xd + kTau * xacc;

@@ -25,7 +25,6 @@ struct StepParams {
   float *total_reward;
   uint32_t *ret_sum;
   uint32_t first;          // 1: accumulators start from zero at this step
-  unsigned long long *global;  // [2] or nullptr
 };
 
 // A whole rollout of T steps in one launch (register-resident).
@@ -50,6 +49,12 @@ hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_
                        hipStream_t stream);
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream);
 hipError_t launch_resident(const RolloutParams &p, hipStream_t stream);
+// global[0] += terminations, global[1] += finished returns of a per-step
+// rollout of T steps, from the episode counters read before (after=false)
+// and after (after=true, extra = n*T) the steps.
+hipError_t launch_episode_sums(const uint32_t *ep_index, const uint32_t *ep_len, uint32_t n,
+                               bool after, unsigned long long extra, unsigned long long *global,
+                               hipStream_t stream);
 constexpr bool kPolicyBuilt = false;
 
 // Unfused level: one kernel per primitive operation; temporaries live in the

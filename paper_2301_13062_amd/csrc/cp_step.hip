@@ -1,16 +1,19 @@
-// cp_step.hip -- initial draw, the fused one-step kernel and the
-// register-resident rollout kernel.
+// cp_step.hip -- initial draw, the fused one-step kernel, the
+// register-resident rollout kernel and the episode-counter sums.
 //
 // Fused step (paper Sec. "Fusion via Memory Movement Optimization"): every
 // operation of one environment step -- action, dynamics, Euler update,
-// termination, reward, reset, bookkeeping -- in one kernel, one environment
-// per lane, each state array read and written once, coalesced (consecutive
-// lanes touch consecutive words of each structure-of-arrays plane).
+// termination, reward, reset, bookkeeping -- in one kernel; each state array
+// is read and written once.  Each lane owns four consecutive environments,
+// so every plane moves as 16-byte accesses (4 bytes for the u8 planes) and a
+// wave covers 1 KiB of each float plane; trajectory outputs are written
+// with non-temporal stores since nothing in the step reads them back.
 //
 // Resident rollout (paper Sec. "Fusion via Unroll" and Sec. "Comparison with
 // CUDA implementation": all steps in one kernel): the state stays in VGPRs
-// for all T steps; per step the wave counts its terminations with a ballot;
-// at the end a wave reduction and one atomic per wave publish the totals.
+// for all T steps; per step the wave counts its terminations with a ballot
+// into a scalar register; at the end the block combines its waves in LDS
+// and one atomic pair per block publishes the totals.
 #include "cp_launch.h"
 
 namespace cp {
@@ -18,6 +21,12 @@ namespace cp {
 namespace {
 
 constexpr int kBlock = 256;
+constexpr int kWaves = kBlock / 64;
+// Below this batch size one environment per lane keeps >= 4 waves per SIMD.
+constexpr uint32_t kVecMinEnvs = 1u << 20;
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *__restrict__ xd,
                                                  float *__restrict__ th, float *__restrict__ thd,
@@ -35,55 +44,163 @@ __global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *_
   ep_len[i] = 0u;
 }
 
-// Publishes a wave's termination count and return sum (lane 0, one atomic
-// pair per wave).  Every lane of the wave must call it.
-__device__ __forceinline__ void wave_publish(unsigned long long *global, uint32_t wave_done,
-                                             uint32_t ret) {
-  const uint32_t rs = wave_sum_u32(ret);
-  if ((threadIdx.x & 63u) == 0u && wave_done != 0u) {
-    atomicAdd(&global[0], (unsigned long long)wave_done);
-    atomicAdd(&global[1], (unsigned long long)rs);
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t lo = __shfl_xor(uint32_t(v), off, 64);
+    const uint32_t hi = __shfl_xor(uint32_t(v >> 32), off, 64);
+    v += (static_cast<unsigned long long>(hi) << 32) | lo;
+  }
+  return v;
+}
+
+// Adds the block's (a, b) sums to global[0], global[1]: waves reduce with
+// lane shuffles, the block through LDS, thread 0 issues one atomic pair.
+// Every thread of the block must call it.
+__device__ __forceinline__ void block_publish(unsigned long long *global, unsigned long long a,
+                                              unsigned long long b, bool a_is_wave_uniform) {
+  __shared__ unsigned long long sa[kWaves], sb[kWaves];
+  if (!a_is_wave_uniform) a = wave_sum_u64(a);
+  b = wave_sum_u64(b);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63u) == 0u) {
+    sa[w] = a;
+    sb[w] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long ta = 0, tb = 0;
+#pragma unroll
+    for (int j = 0; j < kWaves; ++j) {
+      ta += sa[j];
+      tb += sb[j];
+    }
+    if (ta | tb) {
+      atomicAdd(&global[0], ta);
+      atomicAdd(&global[1], tb);
+    }
   }
 }
 
-template <bool kExplicit>
-__global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
-  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
-  const bool valid = i < p.n;
-  uint32_t d = 0u, ret = 0u;
-  if (valid) {
-    const uint32_t env = p.env_base + i;
-    const State s{p.x[i], p.xd[i], p.th[i], p.thd[i]};
-    const uint32_t a = kExplicit ? uint32_t(p.actions[i] != 0) : action_bit(p.kact, env, p.t);
-    State o = dynamics(s, force_of(a));
-    uint32_t len = p.ep_len[i] + 1u;
-    d = terminated(o) ? 1u : 0u;
-    if (d) {
-      ret = len;
-      len = 0u;
-      const uint32_t k = p.ep_index[i] + 1u;
-      p.ep_index[i] = k;
-      o = reset_draw(p.krst, env, k);
-    }
-    p.x[i] = o.x;
-    p.xd[i] = o.xd;
-    p.th[i] = o.th;
-    p.thd[i] = o.thd;
-    p.ep_len[i] = len;
-    if (p.obs) {
-      p.obs[i] = o.x;
-      p.obs[p.n + i] = o.xd;
-      p.obs[2u * p.n + i] = o.th;
-      p.obs[3u * p.n + i] = o.thd;
-    }
-    if (p.reward) p.reward[i] = 1.0f;
-    if (p.done) p.done[i] = uint8_t(d);
-    if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + d;
-    if (p.total_reward) p.total_reward[i] = (p.first ? 0.0f : p.total_reward[i]) + 1.0f;
-    if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
+// One environment's step after its action is known: dynamics, termination,
+// reset.  len is the running episode length (updated); d / ret report the
+// termination and the finished episode's return.
+__device__ __forceinline__ State advance(const StepParams &p, uint32_t i, State s, uint32_t a,
+                                         uint32_t &len, uint32_t &d, uint32_t &ret) {
+  State o = dynamics(s, force_of(a));
+  len += 1u;
+  d = terminated(o) ? 1u : 0u;
+  ret = 0u;
+  if (d) {
+    ret = len;
+    len = 0u;
+    const uint32_t k = p.ep_index[i] + 1u;
+    p.ep_index[i] = k;
+    o = reset_draw(p.krst, p.env_base + i, k);
   }
-  if (p.global) wave_publish(p.global, uint32_t(__popcll(__ballot(d))), ret);
+  return o;
 }
+
+template <bool kExplicit>
+__device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i) {
+  const State s{p.x[i], p.xd[i], p.th[i], p.thd[i]};
+  const uint32_t a = kExplicit ? uint32_t(p.actions[i] != 0) : action_bit(p.kact, p.env_base + i, p.t);
+  uint32_t len = p.ep_len[i], d, ret;
+  const State o = advance(p, i, s, a, len, d, ret);
+  p.x[i] = o.x;
+  p.xd[i] = o.xd;
+  p.th[i] = o.th;
+  p.thd[i] = o.thd;
+  p.ep_len[i] = len;
+  if (p.obs) {
+    __builtin_nontemporal_store(o.x, p.obs + i);
+    __builtin_nontemporal_store(o.xd, p.obs + p.n + i);
+    __builtin_nontemporal_store(o.th, p.obs + 2u * p.n + i);
+    __builtin_nontemporal_store(o.thd, p.obs + 3u * p.n + i);
+  }
+  if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + i);
+  if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + i);
+  if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + d;
+  if (p.total_reward) p.total_reward[i] = (p.first ? 0.0f : p.total_reward[i]) + 1.0f;
+  if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
+}
+
+// Four consecutive environments 4g .. 4g+3 with 16-byte plane accesses.
+template <bool kExplicit>
+__device__ __forceinline__ void fused_four(const StepParams &p, uint32_t g) {
+  const uint32_t i0 = 4u * g;
+  const f32x4 X = *reinterpret_cast<const f32x4 *>(p.x + i0);
+  const f32x4 XD = *reinterpret_cast<const f32x4 *>(p.xd + i0);
+  const f32x4 TH = *reinterpret_cast<const f32x4 *>(p.th + i0);
+  const f32x4 THD = *reinterpret_cast<const f32x4 *>(p.thd + i0);
+  const u32x4 LEN = *reinterpret_cast<const u32x4 *>(p.ep_len + i0);
+  const uint32_t A4 = kExplicit ? *reinterpret_cast<const uint32_t *>(p.actions + i0) : 0u;
+  f32x4 OX, OXD, OTH, OTHD;
+  u32x4 OLEN, RET, D;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const uint32_t i = i0 + uint32_t(k);
+    const uint32_t a = kExplicit ? uint32_t(((A4 >> (8 * k)) & 0xFFu) != 0u)
+                                 : action_bit(p.kact, p.env_base + i, p.t);
+    uint32_t len = LEN[k], d, ret;
+    const State o = advance(p, i, State{X[k], XD[k], TH[k], THD[k]}, a, len, d, ret);
+    OX[k] = o.x;
+    OXD[k] = o.xd;
+    OTH[k] = o.th;
+    OTHD[k] = o.thd;
+    OLEN[k] = len;
+    RET[k] = ret;
+    D[k] = d;
+  }
+  *reinterpret_cast<f32x4 *>(p.x + i0) = OX;
+  *reinterpret_cast<f32x4 *>(p.xd + i0) = OXD;
+  *reinterpret_cast<f32x4 *>(p.th + i0) = OTH;
+  *reinterpret_cast<f32x4 *>(p.thd + i0) = OTHD;
+  *reinterpret_cast<u32x4 *>(p.ep_len + i0) = OLEN;
+  if (p.obs) {
+    __builtin_nontemporal_store(OX, reinterpret_cast<f32x4 *>(p.obs + i0));
+    __builtin_nontemporal_store(OXD, reinterpret_cast<f32x4 *>(p.obs + p.n + i0));
+    __builtin_nontemporal_store(OTH, reinterpret_cast<f32x4 *>(p.obs + 2u * p.n + i0));
+    __builtin_nontemporal_store(OTHD, reinterpret_cast<f32x4 *>(p.obs + 3u * p.n + i0));
+  }
+  if (p.reward) {
+    const f32x4 one = {1.0f, 1.0f, 1.0f, 1.0f};
+    __builtin_nontemporal_store(one, reinterpret_cast<f32x4 *>(p.reward + i0));
+  }
+  if (p.done) {
+    const uint32_t packed = D[0] | (D[1] << 8) | (D[2] << 16) | (D[3] << 24);
+    __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t *>(p.done + i0));
+  }
+  if (p.done_count) {
+    u32x4 *q = reinterpret_cast<u32x4 *>(p.done_count + i0);
+    *q = (p.first ? u32x4{0u, 0u, 0u, 0u} : *q) + D;
+  }
+  if (p.total_reward) {
+    f32x4 *q = reinterpret_cast<f32x4 *>(p.total_reward + i0);
+    const f32x4 one = {1.0f, 1.0f, 1.0f, 1.0f};
+    *q = (p.first ? f32x4{0.f, 0.f, 0.f, 0.f} : *q) + one;
+  }
+  if (p.ret_sum) {
+    u32x4 *q = reinterpret_cast<u32x4 *>(p.ret_sum + i0);
+    *q = (p.first ? u32x4{0u, 0u, 0u, 0u} : *q) + RET;
+  }
+}
+
+template <bool kExplicit, bool kVec>
+__global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
+  const uint32_t g = blockIdx.x * kBlock + threadIdx.x;
+  if (kVec) {
+    if (g < p.n / 4u) fused_four<kExplicit>(p, g);
+  } else {
+    if (g < p.n) fused_one<kExplicit>(p, g);
+  }
+}
+
+// Refill period of the prefetched reset states.  An episode drawn from the
+// reset distribution lasts at least 8 steps, so a lane that used its
+// prefetched start state gets the next one before it can terminate again;
+// the per-lane fallback below keeps results exact for any episode length.
+constexpr uint32_t kRefill = 8u;
 
 template <bool kTraj>
 __global__ __launch_bounds__(kBlock) void k_resident(RolloutParams p) {
@@ -91,47 +208,59 @@ __global__ __launch_bounds__(kBlock) void k_resident(RolloutParams p) {
   const bool valid = i < p.n;
   const uint32_t env = p.env_base + i;
   // Lanes past the end run the loop on a dummy state (the wave stays
-  // converged for the ballots) and store nothing.
+  // converged for the ballots), never terminate and store nothing.
   State s{0.f, 0.f, 0.f, 0.f};
-  uint32_t k = 0u, len = 0u;
+  uint32_t k0 = 0u, len0 = 0u;
   if (valid) {
     s = State{p.x[i], p.xd[i], p.th[i], p.thd[i]};
-    k = p.ep_index[i];
-    len = p.ep_len[i];
+    k0 = p.ep_index[i];
+    len0 = p.ep_len[i];
   }
-  uint32_t n_done = 0u, returns = 0u, wave_done = 0u;
-  float rsum = 0.0f;
+  uint32_t k = k0, len = len0;
+  // Start state of the next episode, drawn ahead of time so that a
+  // termination costs a select; `have` says whether it is drawn yet.
+  State nxt = reset_draw(p.krst, env, k + 1u);
+  bool have = true;
+  unsigned long long wave_done = 0u;
   U2 block{0u, 0u};
   for (uint32_t j = 0; j < p.T; ++j) {
     const uint32_t t = p.t0 + j;
     if (j == 0u || (t & 63u) == 0u) block = threefry2x32(p.kact.a, p.kact.b, env, t >> 6);
     const uint32_t a = action_from_block(block, t);
     State o = dynamics(s, force_of(a));
-    len += 1u;
-    rsum += 1.0f;
     const bool d = valid && terminated(o);
-    if (d) {
-      returns += len;
-      n_done += 1u;
-      len = 0u;
-      k += 1u;
-      o = reset_draw(p.krst, env, k);
-    }
+    k += d ? 1u : 0u;
+    len = d ? 0u : len + 1u;
+    if (d && !have) nxt = reset_draw(p.krst, env, k);  // second termination before a refill
+    if (d) o = nxt;
+    have = have && !d;
     s = o;
     if (kTraj && valid) {
       const size_t base = size_t(j) * p.n + i;
       if (p.obs) {
         const size_t ob = size_t(j) * 4u * p.n + i;
-        p.obs[ob] = s.x;
-        p.obs[ob + p.n] = s.xd;
-        p.obs[ob + 2u * p.n] = s.th;
-        p.obs[ob + 3u * p.n] = s.thd;
+        __builtin_nontemporal_store(s.x, p.obs + ob);
+        __builtin_nontemporal_store(s.xd, p.obs + ob + p.n);
+        __builtin_nontemporal_store(s.th, p.obs + ob + 2u * p.n);
+        __builtin_nontemporal_store(s.thd, p.obs + ob + 3u * p.n);
       }
-      if (p.reward) p.reward[base] = 1.0f;
-      if (p.done) p.done[base] = uint8_t(d);
+      if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + base);
+      if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + base);
     }
-    wave_done += uint32_t(__popcll(__ballot(d)));
+    wave_done += __popcll(__ballot(d));
+    // batched refill: the lanes that used their prefetched state draw the
+    // start state of the episode after the current one
+    if ((j % kRefill) == kRefill - 1u && !have) {
+      nxt = reset_draw(p.krst, env, k + 1u);
+      have = true;
+    }
   }
+  // Over the rollout an environment's terminations are the growth of its
+  // episode index and its finished returns are T + len(start) - len(end);
+  // the summed reward of T steps (1 each, accumulated in binary32) is T up
+  // to 2^24, where the binary32 sum stops growing.
+  const uint32_t n_done = k - k0;
+  const uint32_t returns = p.T + len0 - len;
   if (valid) {
     p.x[i] = s.x;
     p.xd[i] = s.xd;
@@ -140,13 +269,37 @@ __global__ __launch_bounds__(kBlock) void k_resident(RolloutParams p) {
     p.ep_index[i] = k;
     p.ep_len[i] = len;
     if (p.done_count) p.done_count[i] = n_done;
-    if (p.total_reward) p.total_reward[i] = rsum;
+    if (p.total_reward) p.total_reward[i] = float(p.T < (1u << 24) ? p.T : (1u << 24));
     if (p.ret_sum) p.ret_sum[i] = returns;
   }
-  if (p.global) wave_publish(p.global, wave_done, returns);
+  if (p.global) block_publish(p.global, wave_done, valid ? returns : 0u, true);
 }
 
-inline dim3 grid_for(uint32_t n) { return dim3((n + kBlock - 1) / kBlock); }
+// Totals of a per-step rollout from the episode counters: over T steps an
+// environment's terminations are the growth of ep_index and its finished
+// returns are T + ep_len(before) - ep_len(after).  Called once before the
+// steps (after == 0) and once after them (after == 1, extra = n*T); the
+// two calls' contributions add up modulo 2^64 to the exact totals.
+__global__ __launch_bounds__(kBlock) void k_episode_sums(const uint32_t *__restrict__ ep_index,
+                                                         const uint32_t *__restrict__ ep_len,
+                                                         uint32_t n, int after,
+                                                         unsigned long long extra,
+                                                         unsigned long long *global) {
+  unsigned long long sk = 0u, sl = 0u;
+  for (uint32_t i = blockIdx.x * kBlock + threadIdx.x; i < n; i += gridDim.x * kBlock) {
+    sk += ep_index[i];
+    sl += ep_len[i];
+  }
+  const unsigned long long zero = 0u;
+  unsigned long long dk = after ? sk : zero - sk;
+  unsigned long long dl = after ? zero - sl : sl;
+  if (after && blockIdx.x == 0 && threadIdx.x == 0) dl += extra;
+  block_publish(global, dk, dl, false);
+}
+
+inline dim3 grid_for(uint32_t threads) { return dim3((threads + kBlock - 1) / kBlock); }
+
+inline bool al(const void *q, uintptr_t a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; }
 
 }  // namespace
 
@@ -159,10 +312,21 @@ hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_
 }
 
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
-  if (p.actions)
-    hipLaunchKernelGGL(k_fused_step<true>, grid_for(p.n), dim3(kBlock), 0, stream, p);
-  else
-    hipLaunchKernelGGL(k_fused_step<false>, grid_for(p.n), dim3(kBlock), 0, stream, p);
+  // Four environments per lane for large batches when every plane (and
+  // every output plane, offset by multiples of n) is 16-byte aligned; small
+  // batches keep one environment per lane so that enough waves exist.
+  const bool vec = p.n >= kVecMinEnvs && p.n % 4u == 0u && al(p.x, 16) && al(p.xd, 16) && al(p.th, 16) &&
+                   al(p.thd, 16) && al(p.ep_len, 16) && al(p.obs, 16) && al(p.reward, 16) &&
+                   al(p.done, 4) && al(p.actions, 4) && al(p.done_count, 16) &&
+                   al(p.total_reward, 16) && al(p.ret_sum, 16);
+  const dim3 grid = grid_for(vec ? p.n / 4u : p.n);
+  if (p.actions) {
+    if (vec) hipLaunchKernelGGL((k_fused_step<true, true>), grid, dim3(kBlock), 0, stream, p);
+    else hipLaunchKernelGGL((k_fused_step<true, false>), grid, dim3(kBlock), 0, stream, p);
+  } else {
+    if (vec) hipLaunchKernelGGL((k_fused_step<false, true>), grid, dim3(kBlock), 0, stream, p);
+    else hipLaunchKernelGGL((k_fused_step<false, false>), grid, dim3(kBlock), 0, stream, p);
+  }
   return hipGetLastError();
 }
 
@@ -172,6 +336,15 @@ hipError_t launch_resident(const RolloutParams &p, hipStream_t stream) {
     hipLaunchKernelGGL(k_resident<true>, grid_for(p.n), dim3(kBlock), 0, stream, p);
   else
     hipLaunchKernelGGL(k_resident<false>, grid_for(p.n), dim3(kBlock), 0, stream, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_episode_sums(const uint32_t *ep_index, const uint32_t *ep_len, uint32_t n,
+                               bool after, unsigned long long extra, unsigned long long *global,
+                               hipStream_t stream) {
+  const uint32_t blocks = (n + kBlock - 1) / kBlock < 1024u ? (n + kBlock - 1) / kBlock : 1024u;
+  hipLaunchKernelGGL(k_episode_sums, dim3(blocks), dim3(kBlock), 0, stream, ep_index, ep_len, n,
+                     after ? 1 : 0, extra, global);
   return hipGetLastError();
 }
 

@@ -23,7 +23,14 @@ __device__ __forceinline__ float apply(float a, float b) {
   if constexpr (op == Bin::Add) return a + b;
   if constexpr (op == Bin::Sub) return a - b;
   if constexpr (op == Bin::Mul) return a * b;
-  return a / b;
+  return div_rn(a, b);
+}
+
+// x / M, the step's division by the total mass
+__global__ __launch_bounds__(kBlock) void k_div_mass(const float *a, float *out, uint32_t n) {
+  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i >= n) return;
+  out[i] = div_mass(a[i]);
 }
 
 #define CP_EW_INDEX                                   \
@@ -191,23 +198,6 @@ __global__ __launch_bounds__(kBlock) void k_reset_component(U2 key, uint32_t env
   out[i] = reset_value((comp & 1) ? w.b : w.a);
 }
 
-// Sum of the termination flags and of the finished-episode returns, one
-// atomic pair per wave.
-__global__ __launch_bounds__(kBlock) void k_reduce_totals(const uint8_t *f,
-                                                          const uint32_t *ret,
-                                                          unsigned long long *g,
-                                                          uint32_t n) {
-  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
-  const uint32_t d = i < n ? f[i] : 0u;
-  const uint32_t r = i < n ? ret[i] : 0u;
-  const uint32_t nd = uint32_t(__popcll(__ballot(d)));
-  const uint32_t rs = wave_sum_u32(r);
-  if ((threadIdx.x & 63u) == 0u && nd != 0u) {
-    atomicAdd(&g[0], (unsigned long long)nd);
-    atomicAdd(&g[1], (unsigned long long)rs);
-  }
-}
-
 #undef CP_EW_INDEX
 
 // Workspace layout: kF32Temps binary32 planes, then kU32Temps u32 planes,
@@ -255,20 +245,20 @@ hipError_t launch_unfused_step(const StepParams &p, void *workspace, hipStream_t
   hipLaunchKernelGGL(k_sv<Bin::Mul>, g, b, 0, st, kPoleMassLength, f[A_THD2], f[A_T1], n);
   hipLaunchKernelGGL(k_vv<Bin::Mul>, g, b, 0, st, f[A_T1], f[A_SIN], f[A_T2], n);
   hipLaunchKernelGGL(k_vv<Bin::Add>, g, b, 0, st, f[A_FORCE], f[A_T2], f[A_T3], n);
-  hipLaunchKernelGGL(k_vs<Bin::Div>, g, b, 0, st, f[A_T3], kTotalMass, f[A_TEMP], n);
+  hipLaunchKernelGGL(k_div_mass, g, b, 0, st, f[A_T3], f[A_TEMP], n);
   // thacc = (g sin - cos temp) / (l (4/3 - (mp cos^2) / M))
   hipLaunchKernelGGL(k_sv<Bin::Mul>, g, b, 0, st, kGravity, f[A_SIN], f[A_GSIN], n);
   hipLaunchKernelGGL(k_vv<Bin::Mul>, g, b, 0, st, f[A_COS], f[A_TEMP], f[A_CTEMP], n);
   hipLaunchKernelGGL(k_vv<Bin::Sub>, g, b, 0, st, f[A_GSIN], f[A_CTEMP], f[A_NUM], n);
   hipLaunchKernelGGL(k_sv<Bin::Mul>, g, b, 0, st, kMassPole, f[A_COS2], f[A_MC2], n);
-  hipLaunchKernelGGL(k_vs<Bin::Div>, g, b, 0, st, f[A_MC2], kTotalMass, f[A_Q], n);
+  hipLaunchKernelGGL(k_div_mass, g, b, 0, st, f[A_MC2], f[A_Q], n);
   hipLaunchKernelGGL(k_sv<Bin::Sub>, g, b, 0, st, kFourThirds, f[A_Q], f[A_D1], n);
   hipLaunchKernelGGL(k_sv<Bin::Mul>, g, b, 0, st, kHalfLength, f[A_D1], f[A_DEN], n);
   hipLaunchKernelGGL(k_vv<Bin::Div>, g, b, 0, st, f[A_NUM], f[A_DEN], f[A_THACC], n);
   // xacc = temp - ((pml * thacc) * cos) / M
   hipLaunchKernelGGL(k_sv<Bin::Mul>, g, b, 0, st, kPoleMassLength, f[A_THACC], f[A_P1], n);
   hipLaunchKernelGGL(k_vv<Bin::Mul>, g, b, 0, st, f[A_P1], f[A_COS], f[A_P2], n);
-  hipLaunchKernelGGL(k_vs<Bin::Div>, g, b, 0, st, f[A_P2], kTotalMass, f[A_P3], n);
+  hipLaunchKernelGGL(k_div_mass, g, b, 0, st, f[A_P2], f[A_P3], n);
   hipLaunchKernelGGL(k_vv<Bin::Sub>, g, b, 0, st, f[A_TEMP], f[A_P3], f[A_XACC], n);
   // explicit Euler with the old state
   hipLaunchKernelGGL(k_sv<Bin::Mul>, g, b, 0, st, kTau, p.xd, f[A_DX], n);
@@ -322,7 +312,6 @@ hipError_t launch_unfused_step(const StepParams &p, void *workspace, hipStream_t
     if (p.first) hipLaunchKernelGGL(k_fill_u32, g, b, 0, st, 0u, p.ret_sum, n);
     hipLaunchKernelGGL(k_add_u32v, g, b, 0, st, p.ret_sum, u[B_RET], p.ret_sum, n);
   }
-  if (p.global) hipLaunchKernelGGL(k_reduce_totals, g, b, 0, st, c[C_DONE], u[B_RET], p.global, n);
   return hipGetLastError();
 }
 

@@ -90,8 +90,8 @@ def test_init_bit_exact(gpu, n):
 
 
 # --------------------------------------------------------------------------- one step
-def _one_step_case(variant, kind, hashed):
-    n, seed, t = 4099, 9, 70
+def _one_step_case(variant, kind, hashed, n=4099, offset_outputs=False):
+    seed, t = 9, 70
     rng = np.random.default_rng(100 * variant + 10 * (kind == "adversarial") + hashed)
     st4 = synth.states(n, seed=31, kind=kind)
     ep_index = rng.integers(0, 1000, n).astype(np.uint32)
@@ -99,9 +99,10 @@ def _one_step_case(variant, kind, hashed):
     acts = None if hashed else synth.actions(1, n, seed=32)
     s = cp.CartPoleStates(n, variant=variant)
     load(s, st4, ep_index, ep_len, seed, t)
-    obs = torch.empty((4, n), dtype=torch.float32, device="cuda")
-    rew = torch.empty(n, dtype=torch.float32, device="cuda")
-    done = torch.empty(n, dtype=torch.uint8, device="cuda")
+    k = 1 if offset_outputs else 0  # 4-byte offset: no 16-byte accesses possible
+    obs = torch.empty(4 * n + k, dtype=torch.float32, device="cuda")[k:].view(4, n)
+    rew = torch.empty(n + k, dtype=torch.float32, device="cuda")[k:]
+    done = torch.empty(n + k, dtype=torch.uint8, device="cuda")[k:]
     a_dev = None if acts is None else torch.from_numpy(acts[0]).cuda()
     cp.cp_step(s, a_dev, obs, rew, done)
     torch.cuda.synchronize()
@@ -121,18 +122,25 @@ def _one_step_case(variant, kind, hashed):
     return d.mean()
 
 
+# n = 4096 takes the four-environments-per-lane path of the fused kernel,
+# n = 4099 and offset outputs the one-environment-per-lane path.
+SHAPES = [(4099, False), (4096, False), (4096, True)]
+
+
 @pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
 @pytest.mark.parametrize("kind", ["typical", "adversarial"])
-def test_single_step_explicit_actions(gpu, variant, kind):
-    frac = _one_step_case(variant, kind, hashed=False)
+@pytest.mark.parametrize("n,offset", SHAPES)
+def test_single_step_explicit_actions(gpu, variant, kind, n, offset):
+    frac = _one_step_case(variant, kind, hashed=False, n=n, offset_outputs=offset)
     if kind == "adversarial":
         assert frac > 0.05  # the adversarial mix does terminate
 
 
 @pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
 @pytest.mark.parametrize("kind", ["typical", "adversarial"])
-def test_single_step_random_actions(gpu, variant, kind):
-    _one_step_case(variant, kind, hashed=True)
+@pytest.mark.parametrize("n,offset", SHAPES)
+def test_single_step_random_actions(gpu, variant, kind, n, offset):
+    _one_step_case(variant, kind, hashed=True, n=n, offset_outputs=offset)
 
 
 # --------------------------------------------------------------------------- levels agree
