@@ -4,10 +4,12 @@
 // Fused step (paper Sec. "Fusion via Memory Movement Optimization"): every
 // operation of one environment step -- action, dynamics, Euler update,
 // termination, reward, reset, bookkeeping -- in one kernel; each state array
-// is read and written once.  Each lane owns four consecutive environments,
-// so every plane moves as 16-byte accesses (4 bytes for the u8 planes) and a
-// wave covers 1 KiB of each float plane; trajectory outputs are written
-// with non-temporal stores since nothing in the step reads them back.
+// is read and written once, one environment per lane, so a wave reads and
+// writes 256 contiguous bytes of each plane.  Trajectory outputs are written
+// with non-temporal stores since nothing in the step reads them back (on
+// MI355X this measured faster than plain stores, and one environment per
+// lane faster than four per lane with 16-byte accesses, at 65,536 to
+// 16,777,216 environments).
 //
 // Resident rollout (paper Sec. "Fusion via Unroll" and Sec. "Comparison with
 // CUDA implementation": all steps in one kernel): the state stays in VGPRs
@@ -22,11 +24,7 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kWaves = kBlock / 64;
-// Below this batch size one environment per lane keeps >= 4 waves per SIMD.
-constexpr uint32_t kVecMinEnvs = 1u << 20;
 
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *__restrict__ xd,
                                                  float *__restrict__ th, float *__restrict__ thd,
@@ -125,75 +123,10 @@ __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i) {
   if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
 }
 
-// Four consecutive environments 4g .. 4g+3 with 16-byte plane accesses.
 template <bool kExplicit>
-__device__ __forceinline__ void fused_four(const StepParams &p, uint32_t g) {
-  const uint32_t i0 = 4u * g;
-  const f32x4 X = *reinterpret_cast<const f32x4 *>(p.x + i0);
-  const f32x4 XD = *reinterpret_cast<const f32x4 *>(p.xd + i0);
-  const f32x4 TH = *reinterpret_cast<const f32x4 *>(p.th + i0);
-  const f32x4 THD = *reinterpret_cast<const f32x4 *>(p.thd + i0);
-  const u32x4 LEN = *reinterpret_cast<const u32x4 *>(p.ep_len + i0);
-  const uint32_t A4 = kExplicit ? *reinterpret_cast<const uint32_t *>(p.actions + i0) : 0u;
-  f32x4 OX, OXD, OTH, OTHD;
-  u32x4 OLEN, RET, D;
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    const uint32_t i = i0 + uint32_t(k);
-    const uint32_t a = kExplicit ? uint32_t(((A4 >> (8 * k)) & 0xFFu) != 0u)
-                                 : action_bit(p.kact, p.env_base + i, p.t);
-    uint32_t len = LEN[k], d, ret;
-    const State o = advance(p, i, State{X[k], XD[k], TH[k], THD[k]}, a, len, d, ret);
-    OX[k] = o.x;
-    OXD[k] = o.xd;
-    OTH[k] = o.th;
-    OTHD[k] = o.thd;
-    OLEN[k] = len;
-    RET[k] = ret;
-    D[k] = d;
-  }
-  *reinterpret_cast<f32x4 *>(p.x + i0) = OX;
-  *reinterpret_cast<f32x4 *>(p.xd + i0) = OXD;
-  *reinterpret_cast<f32x4 *>(p.th + i0) = OTH;
-  *reinterpret_cast<f32x4 *>(p.thd + i0) = OTHD;
-  *reinterpret_cast<u32x4 *>(p.ep_len + i0) = OLEN;
-  if (p.obs) {
-    __builtin_nontemporal_store(OX, reinterpret_cast<f32x4 *>(p.obs + i0));
-    __builtin_nontemporal_store(OXD, reinterpret_cast<f32x4 *>(p.obs + p.n + i0));
-    __builtin_nontemporal_store(OTH, reinterpret_cast<f32x4 *>(p.obs + 2u * p.n + i0));
-    __builtin_nontemporal_store(OTHD, reinterpret_cast<f32x4 *>(p.obs + 3u * p.n + i0));
-  }
-  if (p.reward) {
-    const f32x4 one = {1.0f, 1.0f, 1.0f, 1.0f};
-    __builtin_nontemporal_store(one, reinterpret_cast<f32x4 *>(p.reward + i0));
-  }
-  if (p.done) {
-    const uint32_t packed = D[0] | (D[1] << 8) | (D[2] << 16) | (D[3] << 24);
-    __builtin_nontemporal_store(packed, reinterpret_cast<uint32_t *>(p.done + i0));
-  }
-  if (p.done_count) {
-    u32x4 *q = reinterpret_cast<u32x4 *>(p.done_count + i0);
-    *q = (p.first ? u32x4{0u, 0u, 0u, 0u} : *q) + D;
-  }
-  if (p.total_reward) {
-    f32x4 *q = reinterpret_cast<f32x4 *>(p.total_reward + i0);
-    const f32x4 one = {1.0f, 1.0f, 1.0f, 1.0f};
-    *q = (p.first ? f32x4{0.f, 0.f, 0.f, 0.f} : *q) + one;
-  }
-  if (p.ret_sum) {
-    u32x4 *q = reinterpret_cast<u32x4 *>(p.ret_sum + i0);
-    *q = (p.first ? u32x4{0u, 0u, 0u, 0u} : *q) + RET;
-  }
-}
-
-template <bool kExplicit, bool kVec>
 __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
-  const uint32_t g = blockIdx.x * kBlock + threadIdx.x;
-  if (kVec) {
-    if (g < p.n / 4u) fused_four<kExplicit>(p, g);
-  } else {
-    if (g < p.n) fused_one<kExplicit>(p, g);
-  }
+  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i < p.n) fused_one<kExplicit>(p, i);
 }
 
 // Refill period of the prefetched reset states.  An episode drawn from the
@@ -299,7 +232,6 @@ __global__ __launch_bounds__(kBlock) void k_episode_sums(const uint32_t *__restr
 
 inline dim3 grid_for(uint32_t threads) { return dim3((threads + kBlock - 1) / kBlock); }
 
-inline bool al(const void *q, uintptr_t a) { return q == nullptr || (reinterpret_cast<uintptr_t>(q) % a) == 0; }
 
 }  // namespace
 
@@ -312,21 +244,10 @@ hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_
 }
 
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
-  // Four environments per lane for large batches when every plane (and
-  // every output plane, offset by multiples of n) is 16-byte aligned; small
-  // batches keep one environment per lane so that enough waves exist.
-  const bool vec = p.n >= kVecMinEnvs && p.n % 4u == 0u && al(p.x, 16) && al(p.xd, 16) && al(p.th, 16) &&
-                   al(p.thd, 16) && al(p.ep_len, 16) && al(p.obs, 16) && al(p.reward, 16) &&
-                   al(p.done, 4) && al(p.actions, 4) && al(p.done_count, 16) &&
-                   al(p.total_reward, 16) && al(p.ret_sum, 16);
-  const dim3 grid = grid_for(vec ? p.n / 4u : p.n);
-  if (p.actions) {
-    if (vec) hipLaunchKernelGGL((k_fused_step<true, true>), grid, dim3(kBlock), 0, stream, p);
-    else hipLaunchKernelGGL((k_fused_step<true, false>), grid, dim3(kBlock), 0, stream, p);
-  } else {
-    if (vec) hipLaunchKernelGGL((k_fused_step<false, true>), grid, dim3(kBlock), 0, stream, p);
-    else hipLaunchKernelGGL((k_fused_step<false, false>), grid, dim3(kBlock), 0, stream, p);
-  }
+  if (p.actions)
+    hipLaunchKernelGGL(k_fused_step<true>, grid_for(p.n), dim3(kBlock), 0, stream, p);
+  else
+    hipLaunchKernelGGL(k_fused_step<false>, grid_for(p.n), dim3(kBlock), 0, stream, p);
   return hipGetLastError();
 }
 
