@@ -69,10 +69,21 @@ typedef struct cp_states {
     uint64_t t;         /* global step counter, advanced by cp_step / cp_rollout   */
     void *stream;       /* hipStream_t the calls are queued on                     */
     const uint16_t *policy_w; /* NULL = random actions; else CP_POLICY_WEIGHTS bf16
-                                 bit patterns of the MLP policy (device memory)    */
+                                 bit patterns of the MLP policy (device memory,
+                                 2-byte aligned), CP_RESIDENT only; see below      */
     void *workspace;          /* CP_UNFUSED temporaries, >= cp_workspace_bytes()  */
     size_t workspace_bytes;
 } cp_states;
+
+/* MLP policy (the paper's "fuse simulation with neural network inference",
+ * Sec. "Future Work"): 4 -> 64 -> 64 -> 2, no biases, tanh on both hidden
+ * layers, action = 1 (push right) iff logit[1] > logit[0].  Weights are
+ * bfloat16, row-major [in][out], concatenated W1[4][64], W2[64][64],
+ * W3[64][2].  The observation is the pre-step state rounded to bfloat16;
+ * products are accumulated in binary32 on the matrix cores; hidden
+ * activations are rounded to bfloat16 before the next layer.  Where two
+ * logits are within the accumulation and rounding noise of each other the
+ * chosen action may differ from an exact evaluation.                        */
 
 /* Rollout outputs; every field may be NULL (= not produced).  Arrays are
  * step-major: obs[t][4][n] (x, x_dot, theta, theta_dot after step t, after

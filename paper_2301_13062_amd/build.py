@@ -9,7 +9,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(OUT_DIR, "libcartpole.so")
 
-SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip"]
+SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip"]
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

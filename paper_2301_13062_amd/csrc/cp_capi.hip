@@ -42,6 +42,8 @@ int check_states(const cp_states *s) {
     return fail(CP_ERR_ALIGN, "state arrays must be 4-byte aligned");
   if (s->variant != CP_UNFUSED && s->variant != CP_FUSED && s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "unknown variant %d", (int)s->variant);
+  if (reinterpret_cast<uintptr_t>(s->policy_w) & 1u)
+    return fail(CP_ERR_ALIGN, "policy weights must be 2-byte aligned");
   return CP_OK;
 }
 
@@ -110,8 +112,6 @@ CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *rewa
   const bool policy = s->policy_w && !actions;
   if (policy && s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
-  if (policy && !cp::kPolicyBuilt)
-    return fail(CP_ERR_UNSUPPORTED, "the MLP policy kernel is not part of this build");
 
   hipError_t err;
   if (s->variant == CP_RESIDENT && !actions) {
@@ -155,8 +155,6 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
     return fail(CP_ERR_ALIGN, "trajectory outputs must be 4-byte aligned (global: 8-byte)");
   if (s->policy_w && s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
-  if (s->policy_w && !cp::kPolicyBuilt)
-    return fail(CP_ERR_UNSUPPORTED, "the MLP policy kernel is not part of this build");
   if (n_steps == 0) return ok();
 
   hipStream_t st = static_cast<hipStream_t>(s->stream);

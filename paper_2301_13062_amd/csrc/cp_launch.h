@@ -48,14 +48,16 @@ hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_
                        uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst,
                        hipStream_t stream);
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream);
+// Register-resident rollout; with p.policy_w set the MLP policy chooses the
+// actions (launch_resident_policy), otherwise the random action stream.
 hipError_t launch_resident(const RolloutParams &p, hipStream_t stream);
+hipError_t launch_resident_policy(const RolloutParams &p, hipStream_t stream);
 // global[0] += terminations, global[1] += finished returns of a per-step
 // rollout of T steps, from the episode counters read before (after=false)
 // and after (after=true, extra = n*T) the steps.
 hipError_t launch_episode_sums(const uint32_t *ep_index, const uint32_t *ep_len, uint32_t n,
                                bool after, unsigned long long extra, unsigned long long *global,
                                hipStream_t stream);
-constexpr bool kPolicyBuilt = false;
 
 // Unfused level: one kernel per primitive operation; temporaries live in the
 // caller's workspace.

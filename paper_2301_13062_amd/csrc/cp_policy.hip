@@ -1,0 +1,157 @@
+// cp_policy.hip -- register-resident rollout whose actions come from a
+// 4-64-64-2 tanh MLP policy evaluated on the matrix cores, the simulation
+// and the network inference fused in one kernel (the paper's first
+// future-work item, Sec. "Future Work").
+//
+// Per step each wave evaluates the policy for its 64 environments as four
+// 16-environment tiles.  Every dense layer is a chain of
+// v_mfma_f32_16x16x16_bf16 with the weights as the A operand (neurons =
+// rows) and the environments as the B operand (columns): lane 16g+c holds
+// A[c][4g..4g+3], B[4g..4g+3][c] and D[4g..4g+3][c].  Since a layer's D
+// layout (4 consecutive neurons of environment c per lane) is exactly the
+// next layer's B layout (4 consecutive K indices of column c), the hidden
+// activations go from accumulator to tanh to bf16 to the next MFMA without
+// leaving the lane.  Only the layer-1 inputs (the observation, gathered from
+// the lane that owns the environment) and the chosen actions (scattered
+// back) cross lanes, through ds_bpermute.  The 8,960 bytes of bf16 weights
+// are staged once per block through LDS into register fragments.
+#include "cp_launch.h"
+#include "cp_resident.h"
+
+namespace cp {
+
+namespace {
+
+typedef short bf16x4 __attribute__((ext_vector_type(4)));  // four bf16 bit patterns
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kIn = 4, kHid = 64, kOut = 2;
+constexpr int kOffW1 = 0, kOffW2 = kIn * kHid, kOffW3 = kOffW2 + kHid * kHid;
+constexpr int kWeights = kOffW3 + kHid * kOut;  // 4480
+static_assert(kWeights == 4480, "weight count");
+
+// tanh in binary32, within about 2 ulp: an odd minimax polynomial in x^2
+// (fitted on [0, 0.625]) below |x| = 0.625, and 1 - 2 / (e^{2|x|} + 1) with
+// the sign of x above, where that form has no cancellation.
+__device__ __forceinline__ float tanh_f32(float x) {
+  const float ax = __builtin_fabsf(x);
+  const float z = x * x;
+  float p = -0x1.75e1c2p-8f;
+  p = __builtin_fmaf(p, z, 0x1.52269ap-6f);
+  p = __builtin_fmaf(p, z, -0x1.b83c5ap-5f);
+  p = __builtin_fmaf(p, z, 0x1.110726p-3f);
+  p = __builtin_fmaf(p, z, -0x1.555532p-2f);
+  const float poly = __builtin_fmaf(x * z, p, x);
+  const float e = __builtin_amdgcn_exp2f(ax * 0x1.715476p+1f);  // 2^(2|x| log2 e)
+  const float r = __builtin_amdgcn_rcpf(e + 1.0f);
+  const float big = __builtin_copysignf(__builtin_fmaf(-2.0f, r, 1.0f), x);
+  return ax < 0.625f ? poly : big;
+}
+
+// binary32 -> bfloat16, round to nearest, ties to even (finite inputs).
+__device__ __forceinline__ uint32_t bf16_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+  return bf16_bits(lo) | (bf16_bits(hi) << 16);
+}
+
+__device__ __forceinline__ bf16x4 as_bf16x4(uint32_t lo, uint32_t hi) {
+  bf16x4 v;
+  v[0] = short(lo & 0xFFFFu);
+  v[1] = short(lo >> 16);
+  v[2] = short(hi & 0xFFFFu);
+  v[3] = short(hi >> 16);
+  return v;
+}
+
+__device__ __forceinline__ bf16x4 tanh_bf16(f32x4 acc) {
+  return as_bf16x4(pack2(tanh_f32(acc[0]), tanh_f32(acc[1])),
+                   pack2(tanh_f32(acc[2]), tanh_f32(acc[3])));
+}
+
+__device__ __forceinline__ f32x4 mma(bf16x4 a, bf16x4 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
+}
+
+struct MlpPolicy {
+  bf16x4 w1[4];     // W1^T rows 16m..16m+15, K = the 4 inputs (lane group 0 only)
+  bf16x4 w2[4][4];  // W2^T tile (rows 16m.., K chunk 16c..)
+  bf16x4 w3[4];     // W3^T rows 0,1 (lanes c < 2), K chunk 16c..
+
+  // Fragments from the staged weights (row-major [in][out] bf16).
+  __device__ __forceinline__ void load(const uint16_t *w) {
+    const uint32_t lane = threadIdx.x & 63u, g = lane >> 4, c = lane & 15u;
+    for (int m = 0; m < 4; ++m) {
+      for (int j = 0; j < 4; ++j)
+        w1[m][j] = g == 0u ? short(w[kOffW1 + j * kHid + 16 * m + c]) : short(0);
+      for (int kc = 0; kc < 4; ++kc)
+        for (int j = 0; j < 4; ++j)
+          w2[m][kc][j] = short(w[kOffW2 + (16 * kc + 4 * g + j) * kHid + 16 * m + c]);
+      for (int j = 0; j < 4; ++j)
+        w3[m][j] = c < 2u ? short(w[kOffW3 + (16 * m + 4 * g + j) * kOut + c]) : short(0);
+    }
+  }
+
+  // Action of the lane's environment for its pre-step state s.  Called by
+  // every lane of the wave.
+  __device__ __forceinline__ uint32_t operator()(uint32_t, uint32_t, const State &s) {
+    const uint32_t lane = threadIdx.x & 63u, g = lane >> 4, c = lane & 15u;
+    const uint32_t o01 = pack2(s.x, s.xd), o23 = pack2(s.th, s.thd);
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    uint32_t bits = 0u;
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      // layer-1 input of environment 16t + c, in lane group 0
+      const int src = int(16 * t + c) * 4;
+      uint32_t b01 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(o01)));
+      uint32_t b23 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(o23)));
+      if (g != 0u) b01 = b23 = 0u;
+      const bf16x4 in = as_bf16x4(b01, b23);
+      bf16x4 h1[4], h2[4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m) h1[m] = tanh_bf16(mma(w1[m], in, zero));
+#pragma unroll
+      for (int m = 0; m < 4; ++m) {
+        f32x4 acc = zero;
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) acc = mma(w2[m][kc], h1[kc], acc);
+        h2[m] = tanh_bf16(acc);
+      }
+      f32x4 logits = zero;
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) logits = mma(w3[kc], h2[kc], logits);
+      // rows 0 and 1 of lane c (group 0): the logits of environment 16t + c
+      bits |= (logits[1] > logits[0] ? 1u : 0u) << t;
+    }
+    // the environment of lane 16g + c is column c of tile g
+    const uint32_t got = uint32_t(__builtin_amdgcn_ds_bpermute(int(c) * 4, int(bits)));
+    return (got >> g) & 1u;
+  }
+};
+
+template <bool kTraj>
+__global__ __launch_bounds__(kResidentBlock) void k_resident_policy(RolloutParams p) {
+  __shared__ uint16_t w[kWeights];
+  for (int idx = threadIdx.x; idx < kWeights; idx += kResidentBlock) w[idx] = p.policy_w[idx];
+  __syncthreads();
+  MlpPolicy policy;
+  policy.load(w);
+  resident_rollout<kTraj>(p, policy);
+}
+
+}  // namespace
+
+hipError_t launch_resident_policy(const RolloutParams &p, hipStream_t stream) {
+  const bool traj = p.obs || p.reward || p.done;
+  const dim3 grid((p.n + kResidentBlock - 1) / kResidentBlock);
+  if (traj)
+    hipLaunchKernelGGL(k_resident_policy<true>, grid, dim3(kResidentBlock), 0, stream, p);
+  else
+    hipLaunchKernelGGL(k_resident_policy<false>, grid, dim3(kResidentBlock), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cp

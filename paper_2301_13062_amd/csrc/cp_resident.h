@@ -1,0 +1,152 @@
+// cp_resident.h -- the register-resident rollout loop shared by the
+// random-action kernel and the MLP-policy kernel.  Internal to the library.
+//
+// One lane owns one environment for all T steps; its state never leaves
+// VGPRs.  Per step: the action (from the policy functor), dynamics,
+// termination; on termination the lane swaps in the start state of its next
+// episode, drawn ahead of time, and the lanes that used theirs draw the next
+// one in a batched pass every kRefill steps.  The wave counts its
+// terminations with a ballot into a scalar register; at the end the block
+// combines its waves in LDS and publishes the totals with one atomic pair.
+#pragma once
+
+#include "cp_launch.h"
+
+namespace cp {
+
+constexpr int kResidentBlock = 256;
+constexpr int kResidentWaves = kResidentBlock / 64;
+
+// Refill period of the prefetched reset states.  An episode drawn from the
+// reset distribution lasts at least 8 steps, so a lane that used its
+// prefetched start state gets the next one before it can terminate again;
+// the per-lane fallback in the loop keeps results exact for any episode
+// length.
+constexpr uint32_t kRefill = 8u;
+
+__device__ __forceinline__ unsigned long long wave_sum_u64(unsigned long long v) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const uint32_t lo = __shfl_xor(uint32_t(v), off, 64);
+    const uint32_t hi = __shfl_xor(uint32_t(v >> 32), off, 64);
+    v += (static_cast<unsigned long long>(hi) << 32) | lo;
+  }
+  return v;
+}
+
+// Adds the block's (a, b) sums to global[0], global[1]: waves reduce with
+// lane shuffles, the block through LDS, thread 0 issues one atomic pair.
+// Every thread of the block must call it.
+template <int kBlockThreads>
+__device__ __forceinline__ void block_publish(unsigned long long *global, unsigned long long a,
+                                              unsigned long long b, bool a_is_wave_uniform) {
+  constexpr int kW = kBlockThreads / 64;
+  __shared__ unsigned long long sa[kW], sb[kW];
+  if (!a_is_wave_uniform) a = wave_sum_u64(a);
+  b = wave_sum_u64(b);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63u) == 0u) {
+    sa[w] = a;
+    sb[w] = b;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned long long ta = 0, tb = 0;
+#pragma unroll
+    for (int j = 0; j < kW; ++j) {
+      ta += sa[j];
+      tb += sb[j];
+    }
+    if (ta | tb) {
+      atomicAdd(&global[0], ta);
+      atomicAdd(&global[1], tb);
+    }
+  }
+}
+
+// Random actions: every 64 steps one generator call yields the next 64
+// action bits of the lane's environment.
+struct HashPolicy {
+  U2 key, block;
+  uint32_t env;
+  __device__ __forceinline__ uint32_t operator()(uint32_t j, uint32_t t, const State &) {
+    if (j == 0u || (t & 63u) == 0u) block = threefry2x32(key.a, key.b, env, t >> 6);
+    return action_from_block(block, t);
+  }
+};
+
+// The loop.  `policy(j, t, s)` returns the action of step t (j-th of this
+// rollout) for the lane's pre-step state s; it is called by every lane of
+// the wave at every step (policies may use cross-lane operations).
+template <bool kTraj, class Policy>
+__device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy &policy) {
+  const uint32_t i = blockIdx.x * kResidentBlock + threadIdx.x;
+  const bool valid = i < p.n;
+  const uint32_t env = p.env_base + i;
+  // Lanes past the end run the loop on a dummy state (the wave stays
+  // converged for the ballots), never terminate and store nothing.
+  State s{0.f, 0.f, 0.f, 0.f};
+  uint32_t k0 = 0u, len0 = 0u;
+  if (valid) {
+    s = State{p.x[i], p.xd[i], p.th[i], p.thd[i]};
+    k0 = p.ep_index[i];
+    len0 = p.ep_len[i];
+  }
+  uint32_t k = k0, len = len0;
+  // Start state of the next episode, drawn ahead of time so that a
+  // termination costs a select; `have` says whether it is drawn yet.
+  State nxt = reset_draw(p.krst, env, k + 1u);
+  bool have = true;
+  unsigned long long wave_done = 0u;
+  for (uint32_t j = 0; j < p.T; ++j) {
+    const uint32_t t = p.t0 + j;
+    const uint32_t a = policy(j, t, s);
+    State o = dynamics(s, force_of(a));
+    const bool d = valid && terminated(o);
+    k += d ? 1u : 0u;
+    len = d ? 0u : len + 1u;
+    if (d && !have) nxt = reset_draw(p.krst, env, k);  // second termination before a refill
+    if (d) o = nxt;
+    have = have && !d;
+    s = o;
+    if (kTraj && valid) {
+      const size_t base = size_t(j) * p.n + i;
+      if (p.obs) {
+        const size_t ob = size_t(j) * 4u * p.n + i;
+        __builtin_nontemporal_store(s.x, p.obs + ob);
+        __builtin_nontemporal_store(s.xd, p.obs + ob + p.n);
+        __builtin_nontemporal_store(s.th, p.obs + ob + 2u * p.n);
+        __builtin_nontemporal_store(s.thd, p.obs + ob + 3u * p.n);
+      }
+      if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + base);
+      if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + base);
+    }
+    wave_done += __popcll(__ballot(d));
+    // batched refill: the lanes that used their prefetched state draw the
+    // start state of the episode after the current one
+    if ((j % kRefill) == kRefill - 1u && !have) {
+      nxt = reset_draw(p.krst, env, k + 1u);
+      have = true;
+    }
+  }
+  // Over the rollout an environment's terminations are the growth of its
+  // episode index and its finished returns are T + len(start) - len(end);
+  // the summed reward of T steps (1 each, accumulated in binary32) is T up
+  // to 2^24, where the binary32 sum stops growing.
+  const uint32_t n_done = k - k0;
+  const uint32_t returns = p.T + len0 - len;
+  if (valid) {
+    p.x[i] = s.x;
+    p.xd[i] = s.xd;
+    p.th[i] = s.th;
+    p.thd[i] = s.thd;
+    p.ep_index[i] = k;
+    p.ep_len[i] = len;
+    if (p.done_count) p.done_count[i] = n_done;
+    if (p.total_reward) p.total_reward[i] = float(p.T < (1u << 24) ? p.T : (1u << 24));
+    if (p.ret_sum) p.ret_sum[i] = returns;
+  }
+  if (p.global) block_publish<kResidentBlock>(p.global, wave_done, valid ? returns : 0u, true);
+}
+
+}  // namespace cp

@@ -115,6 +115,12 @@ def test_unfused_workspace_checks():
     assert call_rollout(h, 2) == cp.CP_ERR_SIZE
 
 
+def test_policy_weights_alignment():
+    h = handle(variant=cp.CP_RESIDENT, policy_w=A + 1)
+    assert call_rollout(h, 2) == cp.CP_ERR_ALIGN
+    assert call_step(h) == cp.CP_ERR_ALIGN
+
+
 def test_policy_needs_resident_variant():
     for v in (cp.CP_FUSED, cp.CP_UNFUSED):
         h = handle(variant=v, policy_w=A, workspace=A,

@@ -1,0 +1,178 @@
+"""MLP-policy rollout (register-resident kernel, dense layers on MFMA)
+against the CPU oracle, through the C ABI.
+
+The action is an argmax of two logits, so where the logits nearly tie the
+GPU's binary32 accumulation on the matrix cores and the oracle's exact sums
+may pick different actions; both are correct evaluations of the policy.
+The tests therefore require (a) that at least 99.9% of environments match
+the oracle exactly in their sequence of terminations, and (b) that every
+environment that differs first diverges at a step where the oracle's two
+logits are within NEAR_TIE of each other.  NEAR_TIE bounds the logit error
+of a few-ulp binary32 difference propagated through one bfloat16 rounding
+flip of a hidden activation (2^-8 relative) times a weight of at most ~0.5.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import paper_2301_13062_amd as cp
+from paper_2301_13062_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+NEAR_TIE = 5e-3
+ROLL_MATCH, ROLL_ABS = 0.999, 1e-3
+
+
+def u32(t):
+    return t.cpu().numpy().view(np.uint32)
+
+
+def weights(seed=0):
+    return synth.policy_weights(seed)
+
+
+def run_policy(w, n, T, seed=0, env_base=0, traj=True, **tk):
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, env_base=env_base, policy_w=wd)
+    cp.cp_init(s, seed)
+    tr = cp.Trajectory(n, T, **tk) if traj else None
+    cp.cp_rollout(s, T, seed, tr)
+    torch.cuda.synchronize()
+    return s, tr
+
+
+def oracle_policy(w, ids, T, seed=0, traj=True):
+    o = O.OracleState(len(ids), np.asarray(ids, np.uint32))
+    O.init(o, seed)
+    out = O.rollout(o, T, policy_w=w, traj=traj)
+    return o, out
+
+
+def first_divergence_margin(w, env, T, seed=0):
+    """Re-run one environment alone on the GPU (its results depend only on
+    its own index) and in the oracle; return the oracle's logit margin at the
+    first step whose action differs, or None if the runs agree."""
+    _, gt = run_policy(w, 1, T, seed=seed, env_base=int(env), stats=False)
+    g_obs = gt.obs.cpu().numpy()[:, :, 0]
+    o = O.OracleState(1, np.array([env], np.uint32))
+    O.init(o, seed)
+    pre = o.state()[:, 0].copy()
+    out = O.rollout(o, T, policy_w=w, traj=True)
+    o_obs = out["obs"][:, :, 0]
+    for j in range(T):
+        if np.abs(g_obs[j].astype(np.float64) - o_obs[j]).max() > 1e-4:
+            _, logits = O.mlp_action(w, pre)
+            return abs(float(logits[1]) - float(logits[0]))
+        pre = o_obs[j]
+    return None
+
+
+def test_policy_single_step(gpu):
+    n, w = 4099, weights(0)
+    st4 = synth.states(n, seed=41, kind="typical")
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, policy_w=wd)
+    for dst, src in zip((s.x, s.x_dot, s.theta, s.theta_dot), st4):
+        dst.copy_(torch.from_numpy(src))
+    s.seed, s.t = 3, 5
+    obs = torch.empty((4, n), device="cuda")
+    cp.cp_step(s, None, obs, None, None)
+    torch.cuda.synchronize()
+    g = obs.cpu().numpy().astype(np.float64)
+    o = O.OracleState(n)
+    o.x[:], o.x_dot[:], o.theta[:], o.theta_dot[:] = st4
+    o.seed, o.t = 3, 5
+    out = O.rollout(o, 1, policy_w=w, traj=True)
+    ref = out["obs"][0].astype(np.float64)
+    close = (np.abs(g - ref) <= np.maximum(1e-6, 1e-5 * np.abs(ref))).all(axis=0)
+    assert close.mean() >= ROLL_MATCH
+    for e in np.nonzero(~close)[0]:
+        _, logits = O.mlp_action(w, st4[:, e])
+        assert abs(logits[1] - logits[0]) < NEAR_TIE, (e, logits)
+    # the policy does act: both actions occur
+    acts = np.array([O.mlp_action(w, st4[:, e])[0] for e in range(0, n, 7)])
+    assert 0.05 < acts.mean() < 0.95
+
+
+def test_policy_rollout_4096x500(gpu):
+    n, T, w = 4096, 500, weights(0)
+    s, tr = run_policy(w, n, T)
+    o, out = oracle_policy(w, np.arange(n), T, traj=("done",))
+    g_done = tr.done.cpu().numpy()
+    match = (g_done == out["done"]).all(axis=0)
+    assert match.mean() >= ROLL_MATCH, match.mean()
+    g = s.state().cpu().numpy().astype(np.float64)
+    assert np.abs(g[:, match] - o.state()[:, match]).max() <= ROLL_ABS
+    assert np.array_equal(u32(tr.done_count)[match], out["done_count"][match])
+    for e in np.nonzero(~match)[0]:
+        margin = first_divergence_margin(w, e, T)
+        assert margin is not None and margin < NEAR_TIE, (e, margin)
+    # a random-weight policy still terminates episodes, but differently
+    # from random actions
+    assert out["done_count"].sum() > 0
+
+
+def test_policy_rollout_4m_x_500_sampled(gpu):
+    n, T, w = 1 << 22, 500, weights(0)
+    s, tr = run_policy(w, n, T, obs=False, reward=False, done=False)
+    dc, rs = u32(tr.done_count), u32(tr.ret_sum)
+    tot = tr.totals.cpu().numpy()
+    assert tot[0] == dc.sum() and tot[1] == rs.sum()
+    assert np.array_equal(rs.astype(np.int64) + u32(s.ep_len), np.full(n, T))
+    rng = np.random.default_rng(7)
+    ids = np.unique(np.concatenate([rng.choice(n, 1024, replace=False), [0, n - 1]]))
+    o, out = oracle_policy(w, ids, T, traj=False)
+    g = s.state().cpu().numpy()[:, ids].astype(np.float64)
+    same = (dc[ids] == out["done_count"]) & (rs[ids] == out["ret_sum"])
+    assert (~same).sum() <= 2  # 99.9% of ~1,000 sampled environments, rounded up
+    assert np.abs(g[:, same] - o.state()[:, same]).max() <= ROLL_ABS
+    for e in ids[~same]:
+        margin = first_divergence_margin(w, e, T)
+        assert margin is not None and margin < NEAR_TIE, (e, margin)
+
+
+def test_policy_zero_weights_always_push_left(gpu):
+    # all logits are 0: the tie picks action 0, i.e. the rollout equals one
+    # with explicit all-zero actions
+    n, T = 1000, 60
+    w = np.zeros(cp.CP_POLICY_WEIGHTS, np.uint16)
+    s, tr = run_policy(w, n, T)
+    ref = cp.CartPoleStates(n, variant=cp.CP_FUSED)
+    cp.cp_init(ref, 0)
+    zeros = torch.zeros(n, dtype=torch.uint8, device="cuda")
+    for _ in range(T):
+        cp.cp_step(ref, zeros)
+    torch.cuda.synchronize()
+    assert torch.equal(s.state(), ref.state())
+    assert torch.equal(s.ep_index, ref.ep_index) and torch.equal(s.ep_len, ref.ep_len)
+
+
+def test_policy_results_depend_only_on_the_environment(gpu):
+    n, T, w = 3000, 120, weights(1)
+    s, tr = run_policy(w, n, T)
+    for e in (0, 63, 64, 1777, n - 1):
+        s1, t1 = run_policy(w, 1, T, env_base=e)
+        assert torch.equal(t1.obs[:, :, 0], tr.obs[:, :, e])
+        assert torch.equal(s1.state()[:, 0], s.state()[:, e])
+    # resume: two halves equal the whole
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    h = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, policy_w=wd)
+    cp.cp_init(h, 0)
+    cp.cp_rollout(h, 50, 0, None)
+    cp.cp_rollout(h, T - 50, 0, None)
+    torch.cuda.synchronize()
+    assert torch.equal(h.state(), s.state())
+
+
+def test_policy_step_equals_rollout(gpu):
+    n, T, w = 777, 30, weights(2)
+    s, tr = run_policy(w, n, T)
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    h = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, policy_w=wd)
+    cp.cp_init(h, 0)
+    for j in range(T):
+        cp.cp_step(h)
+    torch.cuda.synchronize()
+    assert torch.equal(h.state(), s.state())
