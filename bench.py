@@ -9,7 +9,8 @@ fusion comparison is made (unfused per-op chain vs one fused kernel).  A
 Also measured in the same run (extra keys of the same JSON line):
   unfused   the same workload through the one-op-per-kernel chain;
   configs   1,024 x 200 and 1,048,576 x 1,000 register-resident rollouts,
-            16,777,216 x 100 streaming fused steps with full trajectory;
+            16,777,216 x 100 streaming fused steps with full trajectory,
+            4,194,304 x 500 with the MLP policy on the matrix cores;
   roofline  HBM roofline of the fused step kernel: algorithmic bytes per
             launch over the mean launch duration (HIP events around the
             timed region of back-to-back launches, divided by the launches);
@@ -27,7 +28,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
-FP32_VALU_PEAK_TFLOPS = 157.3  # MI355X fp32 vector (packed), TFLOP/s
+# fp32 vector-ALU operation rate: 256 CUs x 128 fp32 lanes per clock x
+# 2.4 GHz (one add, mul, fma or compare per lane per clock; the quoted
+# 157.3 TFLOP/s counts each FMA as two flops).
+VALU_PEAK_TOPS = 256 * 128 * 2.4e9 / 1e12
 METRIC = "env-steps/sec on 1 MI355X; achieved HBM GB/s (or VALU %) vs peak"
 
 # Algorithmic HBM bytes per environment-step of the fused step kernel:
@@ -39,8 +43,38 @@ STEP_BYTES_WITH_OUTPUTS = 61
 STEP_BYTES_STATE_ONLY = 40
 # Algorithmic binary32 operations per environment-step of the dynamics
 # (sin, cos, 2 squares, 15 mul/add/sub/div in the accelerations, 8 in the
-# Euler update, 4 comparisons).
+# Euler update, 4 comparisons), each counted once.
 STEP_FLOPS = 31
+# MLP policy: 2 * (4*64 + 64*64 + 64*2) multiply-adds per environment-step.
+POLICY_FLOPS = 2 * (4 * 64 + 64 * 64 + 64 * 2)
+BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
+
+
+# HBM traffic of one launch of the headline kernel (fused step, 65,536
+# environments) from two rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE,
+# KiB per dispatch), scaled by the same counters' reading for a plain 1 GiB
+# copy (read factor 1.99995, write factor 1.0).  Valid only for the kernel
+# sources they were taken on; any change to them makes the figure null
+# until the counters are taken again.
+COUNTER_SOURCES = ["paper_2301_13062_amd/csrc/cp_step.hip", "paper_2301_13062_amd/csrc/cp_device.h",
+                   "paper_2301_13062_amd/csrc/cp_launch.h", "paper_2301_13062_amd/csrc/cp_resident.h",
+                   "paper_2301_13062_amd/csrc/cp_capi.hip", "paper_2301_13062_amd/build.py"]
+COUNTERS = {"sources_sha256_16": "116af5da52fc73fc",
+            "fused_step_65536": {"fetch_kib": 775.4, "write_kib": 2702.2},
+            "read_factor": 1.99995, "write_factor": 1.0}
+
+
+def measured_traffic_bytes(key):
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in COUNTER_SOURCES:
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
+    if h.hexdigest()[:16] != COUNTERS["sources_sha256_16"]:
+        return None
+    c = COUNTERS[key]
+    return 1024 * (c["fetch_kib"] * COUNTERS["read_factor"] + c["write_kib"] * COUNTERS["write_factor"])
 
 
 def parse():
@@ -51,7 +85,7 @@ def parse():
     ap.add_argument("--quick", action="store_true", help="headline only, no extra configs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", choices=["resident_1024x200", "resident_1048576x1000",
-                                       "streaming_16777216x100", "copy"],
+                                       "streaming_16777216x100", "policy_4194304x500", "copy"],
                     help="run one workload only (for counter collection); prints its JSON")
     return ap.parse_args()
 
@@ -122,6 +156,8 @@ def bench_configs(cp, only=None):
         res["resident_1048576x1000"] = _resident_large(cp)
     if want("streaming_16777216x100"):
         res["streaming_16777216x100"] = _streaming(cp)
+    if want("policy_4194304x500"):
+        res["policy_4194304x500"] = _policy(cp)
     torch.cuda.empty_cache()
     return res
 
@@ -149,8 +185,9 @@ def _resident_large(cp):
     eps = n * T / (mean_ms * 1e-3)
     return {"env_steps_per_s": eps, "ms": mean_ms,
             "roofline": {"bound": "alu", "achieved": eps * STEP_FLOPS / 1e12,
-                         "peak": FP32_VALU_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": eps * STEP_FLOPS / 1e12 / FP32_VALU_PEAK_TFLOPS}}
+                         "peak": VALU_PEAK_TOPS, "unit": "TOP/s",
+                         "frac": eps * STEP_FLOPS / 1e12 / VALU_PEAK_TOPS,
+                         "ops_per_env_step": STEP_FLOPS}}
 
 
 def _streaming(cp):
@@ -172,6 +209,29 @@ def _streaming(cp):
     del s, tr
     torch.cuda.empty_cache()
     return out
+
+
+def _policy(cp):
+    import numpy as np
+    import torch
+
+    from paper_2301_13062_amd import synth
+
+    # 4,194,304 x 500 with the MLP policy (bf16 weights N(0, 1/fan_in), seed 0)
+    n, T = 1 << 22, 500
+    w = torch.from_numpy(synth.policy_weights(0).view(np.int16)).cuda()
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, policy_w=w)
+    cp.cp_init(s, 0)
+    tr = cp.Trajectory(n, T, obs=False, reward=False, done=False)
+    cp.cp_rollout(s, T, 0, tr)
+    wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=3)
+    ms = ev / 3
+    eps = n * T / (ms * 1e-3)
+    tflops = eps * POLICY_FLOPS / 1e12
+    return {"env_steps_per_s": eps, "ms": ms,
+            "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_MFMA_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": tflops / BF16_MFMA_PEAK_TFLOPS,
+                         "flops_per_env_step": POLICY_FLOPS}}
 
 
 def cpu_baseline():
@@ -228,7 +288,8 @@ def main():
                                "random actions, obs/reward/done written every step",
                    "envs": n, "steps_per_launch": 1, "variant": "fused"},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gbs / HBM_PEAK_GBS, "traffic": None,
+                     "frac": gbs / HBM_PEAK_GBS,
+                     "traffic": measured_traffic_bytes("fused_step_65536"),
                      "bytes_per_env_step": STEP_BYTES_WITH_OUTPUTS,
                      "kernel_mean_us": kern_us},
         "unfused": {"env_steps_per_s": head["unfused"]["env_steps_per_s"],
