@@ -68,34 +68,35 @@ void orc_stream_key(uint64_t seed, uint32_t tag, uint32_t key[2])
     orc_threefry2x32((uint32_t)(seed >> 32), (uint32_t)seed, tag, 0u, key);
 }
 
-/* Random action of environment `env` at global step `t`: bit (t mod 64) of
- * the 64-bit block generated on counter (env, t div 64).  Bits 0..31 come
- * from the first output word, 32..63 from the second, least significant
- * first.                                                                   */
+/* Random action of environment `env` at global step `t`: one generator call
+ * on counter (env div 64, t) yields the actions of the 64 environments
+ * 64*(env div 64) .. 64*(env div 64) + 63 at step t; environment env takes
+ * bit (env mod 64), bits 0..31 from the first output word, 32..63 from the
+ * second, least significant first.                                        */
 int orc_action_bit(uint64_t seed, uint32_t env, uint32_t t)
 {
     uint32_t key[2], w[2];
     orc_stream_key(seed, ORC_TAG_ACTION, key);
-    orc_threefry2x32(key[0], key[1], env, t / 64u, w);
-    unsigned j = t % 64u;
+    orc_threefry2x32(key[0], key[1], env / 64u, t, w);
+    unsigned j = env % 64u;
     uint32_t word = (j < 32u) ? w[0] : w[1];
     return (int)((word >> (j % 32u)) & 1u);
 }
 
 /* Start state of episode `episode` of environment `env`: four uniforms in
- * [-0.05, 0.05) (x, x_dot, theta, theta_dot) on a 2^24-point grid.  The four
- * 32-bit words are the outputs on counters (env, 2k) and (env, 2k+1); each
- * word keeps its top 24 bits, is centred and scaled by 0.1 * 2^-24 with one
- * rounding.                                                                */
+ * [-0.05, 0.05) (x, x_dot, theta, theta_dot) on a 2^16-point grid, from one
+ * generator call on counter (env, episode): the low and high 16-bit halves
+ * of the first word, then of the second; each half is centred and scaled by
+ * 0.1 * 2^-16 with one rounding.                                           */
 void orc_reset_state(uint64_t seed, uint32_t env, uint32_t episode, float out[4])
 {
-    uint32_t key[2], u[4];
+    uint32_t key[2], u[2];
     orc_stream_key(seed, ORC_TAG_RESET, key);
-    orc_threefry2x32(key[0], key[1], env, 2u * episode, &u[0]);
-    orc_threefry2x32(key[0], key[1], env, 2u * episode + 1u, &u[2]);
-    const float scale = ldexpf(0.1f, -24);
+    orc_threefry2x32(key[0], key[1], env, episode, u);
+    const uint32_t half[4] = {u[0] & 0xFFFFu, u[0] >> 16, u[1] & 0xFFFFu, u[1] >> 16};
+    const float scale = ldexpf(0.1f, -16);
     for (int j = 0; j < 4; ++j) {
-        int32_t centred = (int32_t)(u[j] >> 8) - (int32_t)(1 << 23);
+        int32_t centred = (int32_t)half[j] - (int32_t)(1 << 15);
         out[j] = (float)centred * scale;
     }
 }

@@ -32,9 +32,9 @@ constexpr float kTau = 0.02f;
 constexpr float kXLimit = 2.4f;
 // 12 degrees in radians, rounded once to binary32 (0x3E567750).
 constexpr float kThetaLimit = 0.209439510239319549f;
-// Reset draws: centred 24-bit integer times 0.1 * 2^-24 (exact power-of-two
+// Reset draws: centred 16-bit integer times 0.1 * 2^-16 (exact power-of-two
 // scaling of 0.1f).
-constexpr float kResetScale = 0x1.99999ap-28f;
+constexpr float kResetScale = 0x1.99999ap-20f;
 
 constexpr uint32_t kTagAction = 1u;
 constexpr uint32_t kTagReset = 2u;
@@ -80,30 +80,51 @@ __host__ __device__ __forceinline__ U2 stream_key(uint64_t seed, uint32_t tag) {
   return threefry2x32(uint32_t(seed >> 32), uint32_t(seed), tag, 0u);
 }
 
-// Random action bit of step t: bit (t mod 64) of the block drawn on counter
-// (env, t / 64); bits 0..31 from the first word, 32..63 from the second.
-__device__ __forceinline__ uint32_t action_from_block(U2 w, uint32_t t) {
-  const uint32_t word = (t & 32u) ? w.b : w.a;
-  return (word >> (t & 31u)) & 1u;
+// Random actions: one generator call on counter (env / 64, t) gives the
+// actions of the 64 environments 64*(env/64) .. +63 at step t; environment
+// env takes bit (env mod 64) -- bits 0..31 from the first word, 32..63 from
+// the second.
+__device__ __forceinline__ uint32_t bit_of_block(U2 w, uint32_t env) {
+  const uint32_t j = env & 63u;
+  return (((j & 32u) ? w.b : w.a) >> (j & 31u)) & 1u;
 }
 
 __device__ __forceinline__ uint32_t action_bit(U2 key, uint32_t env, uint32_t t) {
-  return action_from_block(threefry2x32(key.a, key.b, env, t >> 6), t);
+  return bit_of_block(threefry2x32(key.a, key.b, env >> 6, t), env);
 }
 
-__device__ __forceinline__ float reset_value(uint32_t u) {
-  return float(int32_t(u >> 8) - int32_t(1 << 23)) * kResetScale;
+// The same action for a wave whose lanes hold consecutive environments
+// (lane 0 first; every lane active): the block is computed once per wave on
+// wave-uniform operands (scalar ALU), twice when the wave straddles two
+// 64-environment blocks.
+__device__ __forceinline__ uint32_t action_bit_wave(U2 key, uint32_t env, uint32_t t) {
+  const uint32_t first = __builtin_amdgcn_readfirstlane(env);
+  const uint32_t g0 = first >> 6;
+  U2 w = threefry2x32(key.a, key.b, g0, t);
+  if (first & 63u) {
+    const U2 w1 = threefry2x32(key.a, key.b, g0 + 1u, t);
+    if ((env >> 6) != g0) w = w1;
+  }
+  return bit_of_block(w, env);
+}
+
+// Reset draws: the four 16-bit halves of one generator call, centred and
+// scaled by 0.1 * 2^-16 (an exact power-of-two scaling of 0.1f).
+__device__ __forceinline__ float reset_value(uint32_t h16) {
+  return float(int32_t(h16) - int32_t(1 << 15)) * kResetScale;
 }
 
 struct State {
   float x, xd, th, thd;
 };
 
-// Start state of episode k: words from counters (env, 2k) and (env, 2k+1).
+// Start state of episode k: the generator on counter (env, k); x and x_dot
+// from the low and high halves of the first word, theta and theta_dot from
+// the second.
 __device__ __forceinline__ State reset_draw(U2 key, uint32_t env, uint32_t k) {
-  const U2 p = threefry2x32(key.a, key.b, env, 2u * k);
-  const U2 q = threefry2x32(key.a, key.b, env, 2u * k + 1u);
-  return State{reset_value(p.a), reset_value(p.b), reset_value(q.a), reset_value(q.b)};
+  const U2 w = threefry2x32(key.a, key.b, env, k);
+  return State{reset_value(w.a & 0xFFFFu), reset_value(w.a >> 16), reset_value(w.b & 0xFFFFu),
+               reset_value(w.b >> 16)};
 }
 
 // ---------------------------------------------------------------- sin / cos

@@ -64,14 +64,40 @@ __device__ __forceinline__ void block_publish(unsigned long long *global, unsign
   }
 }
 
-// Random actions: every 64 steps one generator call yields the next 64
-// action bits of the lane's environment.
+// Random actions.  The actions of a 64-environment block at one step are
+// one generator output (see action_bit); every 64 steps each lane computes
+// the block of one of the next 64 steps (lane L: step base + L), and each
+// step reads its block from the owning lane (v_readlane) into scalar
+// registers.  A wave whose environments straddle two blocks computes both.
 struct HashPolicy {
-  U2 key, block;
-  uint32_t env;
+  U2 key;
+  uint32_t env, g0;
+  bool split;
+  U2 b0, b1;  // this lane's blocks for step base + lane
+  uint32_t base;
+
+  __device__ __forceinline__ HashPolicy(U2 k, uint32_t e) : key(k), env(e) {
+    const uint32_t first = __builtin_amdgcn_readfirstlane(e);
+    g0 = first >> 6;
+    split = (first & 63u) != 0u;
+  }
+
   __device__ __forceinline__ uint32_t operator()(uint32_t j, uint32_t t, const State &) {
-    if (j == 0u || (t & 63u) == 0u) block = threefry2x32(key.a, key.b, env, t >> 6);
-    return action_from_block(block, t);
+    if (j == 0u || (t & 63u) == 0u) {
+      base = t & ~63u;
+      const uint32_t step = base + (threadIdx.x & 63u);
+      b0 = threefry2x32(key.a, key.b, g0, step);
+      if (split) b1 = threefry2x32(key.a, key.b, g0 + 1u, step);
+    }
+    const int src = int(t - base);
+    U2 w{uint32_t(__builtin_amdgcn_readlane(int(b0.a), src)),
+         uint32_t(__builtin_amdgcn_readlane(int(b0.b), src))};
+    if (split) {
+      const U2 w1{uint32_t(__builtin_amdgcn_readlane(int(b1.a), src)),
+                  uint32_t(__builtin_amdgcn_readlane(int(b1.b), src))};
+      if ((env >> 6) != g0) w = w1;
+    }
+    return bit_of_block(w, env);
   }
 };
 

@@ -60,9 +60,9 @@ __device__ __forceinline__ State advance(const StepParams &p, uint32_t i, State 
 }
 
 template <bool kExplicit>
-__device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i) {
+__device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
   const State s{p.x[i], p.xd[i], p.th[i], p.thd[i]};
-  const uint32_t a = kExplicit ? uint32_t(p.actions[i] != 0) : action_bit(p.kact, p.env_base + i, p.t);
+  if (kExplicit) a = uint32_t(p.actions[i] != 0);
   uint32_t len = p.ep_len[i], d, ret;
   const State o = advance(p, i, s, a, len, d, ret);
   p.x[i] = o.x;
@@ -86,12 +86,14 @@ __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i) {
 template <bool kExplicit>
 __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
-  if (i < p.n) fused_one<kExplicit>(p, i);
+  // random actions: one block per wave, before any lane leaves
+  const uint32_t a = kExplicit ? 0u : action_bit_wave(p.kact, p.env_base + i, p.t);
+  if (i < p.n) fused_one<kExplicit>(p, i, a);
 }
 
 template <bool kTraj>
 __global__ __launch_bounds__(kResidentBlock) void k_resident(RolloutParams p) {
-  HashPolicy policy{p.kact, U2{0u, 0u}, p.env_base + blockIdx.x * kResidentBlock + threadIdx.x};
+  HashPolicy policy(p.kact, p.env_base + blockIdx.x * kResidentBlock + threadIdx.x);
   resident_rollout<kTraj>(p, policy);
 }
 

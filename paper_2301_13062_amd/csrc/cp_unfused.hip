@@ -193,9 +193,9 @@ __global__ __launch_bounds__(kBlock) void k_reset_component(U2 key, uint32_t env
                                                             int comp, float *out,
                                                             uint32_t n) {
   CP_EW_INDEX
-  const uint32_t env = env_base + i;
-  const U2 w = threefry2x32(key.a, key.b, env, 2u * ep[i] + uint32_t(comp >> 1));
-  out[i] = reset_value((comp & 1) ? w.b : w.a);
+  const U2 w = threefry2x32(key.a, key.b, env_base + i, ep[i]);
+  const uint32_t word = (comp & 2) ? w.b : w.a;
+  out[i] = reset_value((comp & 1) ? word >> 16 : word & 0xFFFFu);
 }
 
 #undef CP_EW_INDEX

@@ -50,9 +50,11 @@ def test_action_stream_balanced_and_uncorrelated():
     a = np.array([[O.action_bit(0, e, t) for t in range(steps)] for e in range(envs)], np.float64)
     n = a.size
     assert abs(a.mean() - 0.5) < 5 * 0.5 / math.sqrt(n)
-    # neighbouring steps and neighbouring environments are uncorrelated
+    # neighbouring steps and neighbouring environments (inside one 64-env
+    # block and across blocks) are uncorrelated
     s = 2 * a - 1
-    for c in ((s[:, 1:] * s[:, :-1]).mean(), (s[1:, :] * s[:-1, :]).mean()):
+    for c in ((s[:, 1:] * s[:, :-1]).mean(), (s[1:, :] * s[:-1, :]).mean(),
+              (s[64:, :] * s[:-64, :]).mean(), (s[32:, :] * s[:-32, :]).mean()):
         assert abs(c) < 5 / math.sqrt(n)
     # different seeds give different streams
     b = np.array([O.action_bit(1, e, t) for e in range(4) for t in range(64)])
@@ -65,11 +67,12 @@ def test_reset_draw_grid_range_uniformity():
     vals = np.array([O.reset_state(7, e, k) for e in range(400) for k in range(10)], np.float64)
     assert vals.shape == (4000, 4)
     assert vals.min() >= -0.05000001 and vals.max() < 0.05
-    step = float(np.ldexp(np.float32(0.1), -24))
+    step = float(np.ldexp(np.float32(0.1), -16))
     q = np.round(vals / step)
-    # each value is a point of the 2^24-point grid, rounded once to binary32
+    # each value is a point of the 2^16-point grid, rounded once to binary32
     assert np.array_equal((q * step).astype(np.float32).astype(np.float64), vals)
-    assert np.all((q >= -2 ** 23) & (q < 2 ** 23))
+    assert np.all((q >= -2 ** 15) & (q < 2 ** 15))
+    assert len(np.unique(q)) > 10000                           # the grid is used finely
     for j in range(4):                                       # each component uniform
         assert stats.kstest(vals[:, j], stats.uniform(loc=-0.05, scale=0.1).cdf).pvalue > 1e-4
     c = np.corrcoef(vals.T)
