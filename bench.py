@@ -34,13 +34,17 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 VALU_PEAK_TOPS = 256 * 128 * 2.4e9 / 1e12
 METRIC = "env-steps/sec on 1 MI355X; achieved HBM GB/s (or VALU %) vs peak"
 
-# Algorithmic HBM bytes per environment-step of the fused step kernel:
-# reads x, x_dot, theta, theta_dot, ep_len (20 B); writes the same (20 B)
-# plus obs (16 B), reward (4 B) and done (1 B).  The episode index is read
-# and written only on termination (about 4.5% of steps) and is not counted.
+# Algorithmic HBM bytes per environment-step of the fused step kernel in a
+# rollout that writes the trajectory.  Small batches (65,536): reads x,
+# x_dot, theta, theta_dot, ep_len (20 B); writes them (20 B) plus obs (16 B),
+# reward (4 B) and done (1 B).  Large batches (from 2^21 environments) read
+# the state from the previous step's obs plane and write it only there:
+# reads 20 B, writes obs, ep_len, reward, done (25 B); the first step reads,
+# and the last writes, the state arrays (16 B once per rollout).  The
+# episode index is read and written only on termination (about 4.5% of
+# steps) and is not counted.
 STEP_BYTES_WITH_OUTPUTS = 61
-# Same kernel without per-step outputs (state round trip only).
-STEP_BYTES_STATE_ONLY = 40
+STEP_BYTES_TRAJ_LARGE = 45
 # Algorithmic binary32 operations per environment-step of the dynamics
 # (sin, cos, 2 squares, 15 mul/add/sub/div in the accelerations, 8 in the
 # Euler update, 4 comparisons), each counted once.
@@ -59,8 +63,8 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 COUNTER_SOURCES = ["paper_2301_13062_amd/csrc/cp_step.hip", "paper_2301_13062_amd/csrc/cp_device.h",
                    "paper_2301_13062_amd/csrc/cp_launch.h", "paper_2301_13062_amd/csrc/cp_resident.h",
                    "paper_2301_13062_amd/csrc/cp_capi.hip", "paper_2301_13062_amd/build.py"]
-COUNTERS = {"sources_sha256_16": "116af5da52fc73fc",
-            "fused_step_65536": {"fetch_kib": 775.4, "write_kib": 2702.2},
+COUNTERS = {"sources_sha256_16": "5ced128ceae1e378",
+            "fused_step_65536": {"fetch_kib": 776.4, "write_kib": 2702.2},
             "read_factor": 1.99995, "write_factor": 1.0}
 
 
@@ -201,11 +205,11 @@ def _streaming(cp):
     cp.cp_rollout(s, T, 0, tr)
     wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=3)
     mean_ms = ev / (3 * T)  # per launch: T back-to-back step kernels per rollout
-    gbs = STEP_BYTES_WITH_OUTPUTS * n / (mean_ms * 1e-3) / 1e9
+    gbs = STEP_BYTES_TRAJ_LARGE * n / (mean_ms * 1e-3) / 1e9
     out = {"env_steps_per_s": n * T * 3 / (ev * 1e-3), "ms": ev / 3,
            "kernel_mean_us": mean_ms * 1e3,
            "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": STEP_BYTES_WITH_OUTPUTS}}
+                        "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": STEP_BYTES_TRAJ_LARGE}}
     del s, tr
     torch.cuda.empty_cache()
     return out

@@ -14,6 +14,8 @@ namespace {
 
 thread_local char g_err[512];
 
+constexpr size_t kObsStateMinEnvs = size_t(1) << 21;
+
 int fail(int code, const char *fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -72,10 +74,10 @@ int hip_status(hipError_t e, const char *what) {
 
 cp::StepParams step_params(const cp_states *s, uint64_t act_seed) {
   cp::StepParams p{};
-  p.x = s->x;
-  p.xd = s->x_dot;
-  p.th = s->theta;
-  p.thd = s->theta_dot;
+  p.xi = p.x = s->x;
+  p.xdi = p.xd = s->x_dot;
+  p.thi = p.th = s->theta;
+  p.thdi = p.thd = s->theta_dot;
   p.ep_index = s->ep_index;
   p.ep_len = s->ep_len;
   p.n = uint32_t(s->n);
@@ -181,12 +183,33 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
                                                      tr.global, st),
                              "cp_rollout totals"))
         return e;
+    // With an obs trajectory the fused step reads its state from the
+    // previous step's obs plane and writes the state arrays only at the
+    // last step: the trajectory already holds every intermediate state.
+    // Used for batches whose state does not stay in the caches between
+    // launches (below that size the state arrays are re-read from cache,
+    // while the trajectory is written past it).
+    const bool obs_state = s->variant == CP_FUSED && tr.obs && n >= kObsStateMinEnvs;
     for (int64_t j = 0; j < n_steps; ++j) {
       p.t = uint32_t(s->t + uint64_t(j));
       p.first = j == 0;
       p.obs = tr.obs ? tr.obs + size_t(j) * 4u * n : nullptr;
       p.reward = tr.reward ? tr.reward + size_t(j) * n : nullptr;
       p.done = tr.done ? tr.done + size_t(j) * n : nullptr;
+      if (obs_state) {
+        if (j > 0) {
+          const float *prev = tr.obs + size_t(j - 1) * 4u * n;
+          p.xi = prev;
+          p.xdi = prev + n;
+          p.thi = prev + 2u * n;
+          p.thdi = prev + 3u * n;
+        }
+        const bool last = j == n_steps - 1;
+        p.x = last ? s->x : nullptr;
+        p.xd = last ? s->x_dot : nullptr;
+        p.th = last ? s->theta : nullptr;
+        p.thd = last ? s->theta_dot : nullptr;
+      }
       hipError_t err = (s->variant == CP_UNFUSED) ? cp::launch_unfused_step(p, s->workspace, st)
                                                   : cp::launch_fused_step(p, st);
       if (int e = hip_status(err, "cp_rollout launch")) {

@@ -12,6 +12,9 @@ namespace cp {
 
 // Batch state and the per-step outputs of one step (fused or unfused).
 struct StepParams {
+  // state read by the step, and state written (nullptr: not written, when a
+  // trajectory's obs plane already holds it); usually the same arrays
+  const float *xi, *xdi, *thi, *thdi;
   float *x, *xd, *th, *thd;
   uint32_t *ep_index, *ep_len;
   uint32_t n, env_base;

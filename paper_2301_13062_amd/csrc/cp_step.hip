@@ -61,14 +61,16 @@ __device__ __forceinline__ State advance(const StepParams &p, uint32_t i, State 
 
 template <bool kExplicit>
 __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
-  const State s{p.x[i], p.xd[i], p.th[i], p.thd[i]};
+  const State s{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
   if (kExplicit) a = uint32_t(p.actions[i] != 0);
   uint32_t len = p.ep_len[i], d, ret;
   const State o = advance(p, i, s, a, len, d, ret);
-  p.x[i] = o.x;
-  p.xd[i] = o.xd;
-  p.th[i] = o.th;
-  p.thd[i] = o.thd;
+  if (p.x) {
+    p.x[i] = o.x;
+    p.xd[i] = o.xd;
+    p.th[i] = o.th;
+    p.thd[i] = o.thd;
+  }
   p.ep_len[i] = len;
   if (p.obs) {
     __builtin_nontemporal_store(o.x, p.obs + i);

@@ -254,6 +254,20 @@ def test_rollout_16m_x_100_streaming_sampled(gpu):
     torch.cuda.empty_cache()
 
 
+def test_large_batch_fused_trajectory_equals_resident(gpu):
+    # From 2^21 environments the fused rollout reads each step's state from
+    # the previous step's obs plane; it must still match the resident kernel
+    # bit for bit (and leave the final state in the state arrays).
+    n, T = (1 << 21) + 37, 20
+    fs, ft = run(cp.CP_FUSED, n, T, seed=4, act_seed=9, stats=False)
+    rs, rt = run(cp.CP_RESIDENT, n, T, seed=4, act_seed=9, stats=False)
+    assert torch.equal(fs.state(), rs.state())
+    assert torch.equal(fs.ep_index, rs.ep_index) and torch.equal(fs.ep_len, rs.ep_len)
+    for f in ("obs", "reward", "done", "totals"):
+        assert torch.equal(getattr(ft, f), getattr(rt, f)), f
+    assert torch.equal(ft.obs[-1], fs.state())
+
+
 # --------------------------------------------------------------------------- invariances
 @pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
 def test_resume_and_sharding_bit_exact(gpu, variant):
