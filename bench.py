@@ -136,6 +136,28 @@ def bench_headline(cp, K, W):
     return n, out
 
 
+UNROLL_LADDER = (1, 2, 5, 10, 20, 50, 100, 250, 1000)
+
+
+def bench_unroll(cp, K=1000):
+    """The headline workload run by the register-resident kernel with k
+    steps per launch (the paper's scan unroll factor, Sec. "Fusion via
+    Unroll"): the state stays in registers for k steps and goes through HBM
+    between launches.  Random actions, no per-step outputs."""
+    n = 65536
+    out = {}
+    for k in UNROLL_LADDER:
+        s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, steps_per_launch=k)
+        cp.cp_init(s, 0)
+        cp.cp_rollout(s, min(K, 10 * k), 0, None)
+        wall, ev = timed(lambda: cp.cp_rollout(s, K, 0, None))
+        out[str(k)] = {"us_per_step": wall * 1e3 / K, "env_steps_per_s": n * K / (wall * 1e-3)}
+    best = min(out, key=lambda k: out[k]["us_per_step"])
+    return {"envs": n, "steps": K, "ladder": out, "best_steps_per_launch": int(best),
+            "speedup_best_vs_1": out["1"]["us_per_step"] / out[best]["us_per_step"],
+            "speedup_10_vs_1": out["1"]["us_per_step"] / out["10"]["us_per_step"]}
+
+
 def bench_copy():
     """A plain 1 GiB copy-like elementwise kernel (reads 1 GiB, writes 1 GiB):
     the reference for scaling HBM byte counters."""
@@ -302,6 +324,7 @@ def main():
     }
     if not args.quick:
         line["configs"] = bench_configs(cp)
+        line["unroll"] = bench_unroll(cp)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline()
     print(json.dumps(line))

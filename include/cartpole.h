@@ -73,6 +73,11 @@ typedef struct cp_states {
                                  2-byte aligned), CP_RESIDENT only; see below      */
     void *workspace;          /* CP_UNFUSED temporaries, >= cp_workspace_bytes()  */
     size_t workspace_bytes;
+    int64_t steps_per_launch; /* CP_RESIDENT rollouts: steps per kernel launch,
+                                 the state going through HBM between launches
+                                 (the paper's scan unroll factor); 0 = all the
+                                 rollout's steps in one launch.  Results do not
+                                 depend on it.                                  */
 } cp_states;
 
 /* MLP policy (the paper's "fuse simulation with neural network inference",
@@ -118,8 +123,9 @@ int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *reward, uin
  * stream of `seed` (or the MLP policy when s->policy_w is set), then
  * s->t += n_steps.  n_steps == 0 is a no-op.  Equivalent, bit for bit, to
  * n_steps calls of cp_step with the same action source.  traj may be NULL.
- * CP_UNFUSED and CP_FUSED launch one step at a time; CP_RESIDENT launches a
- * single kernel for the whole rollout.                                      */
+ * CP_UNFUSED and CP_FUSED launch one step at a time; CP_RESIDENT launches
+ * ceil(n_steps / steps_per_launch) kernels (one when steps_per_launch is 0).
+ * steps_per_launch < 0 is CP_ERR_SIZE.                                      */
 int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
 
 /* Bytes of workspace CP_UNFUSED needs for n environments (0 for the other

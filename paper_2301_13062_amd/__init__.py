@@ -32,7 +32,8 @@ class cp_states(ctypes.Structure):
                 ("ep_index", _p), ("ep_len", _p), ("n", ctypes.c_int64),
                 ("env_base", ctypes.c_uint32), ("variant", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("t", ctypes.c_uint64), ("stream", _p),
-                ("policy_w", _p), ("workspace", _p), ("workspace_bytes", ctypes.c_size_t)]
+                ("policy_w", _p), ("workspace", _p), ("workspace_bytes", ctypes.c_size_t),
+                ("steps_per_launch", ctypes.c_int64)]
 
 
 class cp_traj(ctypes.Structure):
@@ -88,7 +89,7 @@ class CartPoleStates:
     """
 
     def __init__(self, n, variant=CP_FUSED, device="cuda", env_base=0, policy_w=None,
-                 workspace=None):
+                 workspace=None, steps_per_launch=0):
         self.n, self.env_base = int(n), int(env_base)
         self.variant = VARIANTS.get(variant, variant)
         f32 = dict(dtype=torch.float32, device=device)
@@ -102,6 +103,7 @@ class CartPoleStates:
             nbytes = cp_workspace_bytes(self.n, CP_UNFUSED)
             self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
         self.seed, self.t = 0, 0
+        self.steps_per_launch = int(steps_per_launch)
         self.stream = None  # None = torch's current stream at call time
 
     def handle(self):
@@ -110,7 +112,8 @@ class CartPoleStates:
                       _ptr(self.ep_index), _ptr(self.ep_len), self.n, self.env_base,
                       self.variant, self.seed, self.t, st.cuda_stream, _ptr(self.policy_w),
                       _ptr(self.workspace),
-                      0 if self.workspace is None else self.workspace.numel())
+                      0 if self.workspace is None else self.workspace.numel(),
+                      self.steps_per_launch)
         return h
 
     def _sync_back(self, h):

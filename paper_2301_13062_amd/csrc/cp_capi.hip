@@ -157,6 +157,8 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
     return fail(CP_ERR_ALIGN, "trajectory outputs must be 4-byte aligned (global: 8-byte)");
   if (s->policy_w && s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
+  if (s->steps_per_launch < 0)
+    return fail(CP_ERR_SIZE, "steps_per_launch = %lld is negative", (long long)s->steps_per_launch);
   if (n_steps == 0) return ok();
 
   hipStream_t st = static_cast<hipStream_t>(s->stream);
@@ -167,12 +169,23 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
     p.x = sp.x; p.xd = sp.xd; p.th = sp.th; p.thd = sp.thd;
     p.ep_index = sp.ep_index; p.ep_len = sp.ep_len;
     p.n = sp.n; p.env_base = sp.env_base; p.kact = sp.kact; p.krst = sp.krst;
-    p.t0 = sp.t; p.T = uint32_t(n_steps);
     p.policy_w = s->policy_w;
-    p.obs = tr.obs; p.reward = tr.reward; p.done = tr.done;
     p.done_count = tr.done_count; p.total_reward = tr.total_reward; p.ret_sum = tr.ret_sum;
     p.global = tr.global;
-    if (int e = hip_status(cp::launch_resident(p, st), "cp_rollout launch")) return e;
+    const int64_t chunk = s->steps_per_launch > 0 ? s->steps_per_launch : n_steps;
+    for (int64_t j = 0; j < n_steps; j += chunk) {
+      const int64_t len = chunk < n_steps - j ? chunk : n_steps - j;
+      p.t0 = uint32_t(s->t + uint64_t(j));
+      p.T = uint32_t(len);
+      p.first = j == 0;
+      p.obs = tr.obs ? tr.obs + size_t(j) * 4u * n : nullptr;
+      p.reward = tr.reward ? tr.reward + size_t(j) * n : nullptr;
+      p.done = tr.done ? tr.done + size_t(j) * n : nullptr;
+      if (int e = hip_status(cp::launch_resident(p, st), "cp_rollout launch")) {
+        s->t += uint64_t(j);  // steps already queued stay counted
+        return e;
+      }
+    }
   } else {
     cp::StepParams p = step_params(s, seed);
     p.done_count = tr.done_count;

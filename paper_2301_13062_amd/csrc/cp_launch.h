@@ -45,6 +45,7 @@ struct RolloutParams {
   float *total_reward;       // [n]
   uint32_t *ret_sum;         // [n]
   unsigned long long *global;
+  uint32_t first;            // 1: per-env statistics start at this launch
 };
 
 hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_index,

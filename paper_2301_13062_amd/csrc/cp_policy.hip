@@ -48,23 +48,22 @@ __device__ __forceinline__ float tanh_f32(float x) {
   return ax < 0.625f ? poly : big;
 }
 
-// binary32 -> bfloat16, round to nearest, ties to even (finite inputs).
-__device__ __forceinline__ uint32_t bf16_bits(float f) {
-  const uint32_t u = __float_as_uint(f);
-  return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
+// Two binary32 values -> two bfloat16 (round to nearest, ties to even) in
+// one dword, low half first: one v_cvt_pk_bf16_f32.
 __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
-  return bf16_bits(lo) | (bf16_bits(hi) << 16);
+  bf16x2 v;
+  v[0] = static_cast<__bf16>(lo);
+  v[1] = static_cast<__bf16>(hi);
+  return __builtin_bit_cast(uint32_t, v);
 }
 
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Two dwords of packed bfloat16 pairs as one MFMA operand (no data movement).
 __device__ __forceinline__ bf16x4 as_bf16x4(uint32_t lo, uint32_t hi) {
-  bf16x4 v;
-  v[0] = short(lo & 0xFFFFu);
-  v[1] = short(lo >> 16);
-  v[2] = short(hi & 0xFFFFu);
-  v[3] = short(hi >> 16);
-  return v;
+  return __builtin_bit_cast(bf16x4, u32x2{lo, hi});
 }
 
 __device__ __forceinline__ bf16x4 tanh_bf16(f32x4 acc) {

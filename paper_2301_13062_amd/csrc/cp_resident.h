@@ -168,9 +168,16 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
     p.thd[i] = s.thd;
     p.ep_index[i] = k;
     p.ep_len[i] = len;
-    if (p.done_count) p.done_count[i] = n_done;
-    if (p.total_reward) p.total_reward[i] = float(p.T < (1u << 24) ? p.T : (1u << 24));
-    if (p.ret_sum) p.ret_sum[i] = returns;
+    // A rollout split over several launches adds to what the earlier
+    // launches wrote; the reward sum keeps the semantics of adding 1.0f once
+    // per step in binary32 (exact up to 2^24, constant from there on).
+    if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + n_done;
+    if (p.total_reward) {
+      const float prev = p.first ? 0.0f : p.total_reward[i];
+      const float cap = float(1u << 24);
+      p.total_reward[i] = prev >= cap ? prev : __builtin_fminf(prev + float(p.T), cap);
+    }
+    if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + returns;
   }
   if (p.global) block_publish<kResidentBlock>(p.global, wave_done, valid ? returns : 0u, true);
 }

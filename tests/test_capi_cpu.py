@@ -90,6 +90,11 @@ def test_step_counter_range():
     assert call_rollout(handle(), -1) == cp.CP_ERR_SIZE
 
 
+def test_negative_steps_per_launch():
+    h = handle(variant=cp.CP_RESIDENT, steps_per_launch=-1)
+    assert call_rollout(h, 3) == cp.CP_ERR_SIZE and h.t == 7
+
+
 def test_rollout_zero_steps_is_a_noop():
     h = handle()
     assert call_rollout(h, 0) == cp.CP_OK

@@ -268,6 +268,23 @@ def test_large_batch_fused_trajectory_equals_resident(gpu):
     assert torch.equal(ft.obs[-1], fs.state())
 
 
+@pytest.mark.parametrize("k", [1, 3, 7, 64])
+def test_resident_steps_per_launch_bit_exact(gpu, k):
+    # k steps per launch (state through HBM between launches, the paper's
+    # unroll factor) gives exactly the single-launch rollout
+    n, T = 3001, 150
+    ref, rt = run(cp.CP_RESIDENT, n, T, seed=5, act_seed=6)
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, steps_per_launch=k)
+    cp.cp_init(s, 5)
+    tr = cp.Trajectory(n, T)
+    cp.cp_rollout(s, T, 6, tr)
+    torch.cuda.synchronize()
+    assert all(np.array_equal(x, y) for x, y in zip(gpu_state(s), gpu_state(ref)))
+    for f in ("obs", "reward", "done", "done_count", "total_reward", "ret_sum", "totals"):
+        assert torch.equal(getattr(tr, f), getattr(rt, f)), f
+    assert s.t == T
+
+
 # --------------------------------------------------------------------------- invariances
 @pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
 def test_resume_and_sharding_bit_exact(gpu, variant):

@@ -166,6 +166,20 @@ def test_policy_results_depend_only_on_the_environment(gpu):
     assert torch.equal(h.state(), s.state())
 
 
+def test_policy_steps_per_launch(gpu):
+    n, T, w = 1000, 90, weights(3)
+    s, tr = run_policy(w, n, T)
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    h = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, policy_w=wd, steps_per_launch=7)
+    cp.cp_init(h, 0)
+    ht = cp.Trajectory(n, T)
+    cp.cp_rollout(h, T, 0, ht)
+    torch.cuda.synchronize()
+    assert torch.equal(h.state(), s.state())
+    for f in ("obs", "done", "done_count", "ret_sum", "total_reward", "totals"):
+        assert torch.equal(getattr(ht, f), getattr(tr, f)), f
+
+
 def test_policy_step_equals_rollout(gpu):
     n, T, w = 777, 30, weights(2)
     s, tr = run_policy(w, n, T)
