@@ -8,6 +8,8 @@ fusion comparison is made (unfused per-op chain vs one fused kernel).  A
 
 Also measured in the same run (extra keys of the same JSON line):
   unfused   the same workload through the one-op-per-kernel chain;
+  concat    the same workload split into two kernels at a concatenation of
+            the updated state (the paper's baseline before "no concat");
   configs   1,024 x 200 and 1,048,576 x 1,000 register-resident rollouts,
             16,777,216 x 100 streaming fused steps with full trajectory,
             4,194,304 x 500 with the MLP policy on the matrix cores;
@@ -120,7 +122,8 @@ def bench_headline(cp, K, W):
 
     n = 65536
     out = {}
-    for name, variant in (("fused", cp.CP_FUSED), ("unfused", cp.CP_UNFUSED)):
+    for name, variant in (("fused", cp.CP_FUSED), ("concat", cp.CP_CONCAT),
+                          ("unfused", cp.CP_UNFUSED)):
         s = cp.CartPoleStates(n, variant=variant)
         cp.cp_init(s, 0)
         warm = cp.Trajectory(n, W, stats=False, totals=False)
@@ -321,6 +324,9 @@ def main():
         "unfused": {"env_steps_per_s": head["unfused"]["env_steps_per_s"],
                     "us_per_step": head["unfused"]["us_per_step"]},
         "fusion_speedup": fused["env_steps_per_s"] / head["unfused"]["env_steps_per_s"],
+        "concat": {"env_steps_per_s": head["concat"]["env_steps_per_s"],
+                   "us_per_step": head["concat"]["us_per_step"]},
+        "no_concat_speedup": fused["env_steps_per_s"] / head["concat"]["env_steps_per_s"],
     }
     if not args.quick:
         line["configs"] = bench_configs(cp)

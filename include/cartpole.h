@@ -43,6 +43,9 @@ extern "C" {
 #define CP_UNFUSED 0  /* one kernel per primitive operation, temporaries in HBM      */
 #define CP_FUSED 1    /* one kernel per step, state read and written once per step  */
 #define CP_RESIDENT 2 /* one kernel per rollout, state held in registers            */
+#define CP_CONCAT 3   /* two kernels per step split at an [n][4] concatenation of the
+                         updated state in the workspace (the paper's baseline before
+                         its "no concat" change)                                      */
 
 #define CP_OK 0
 #define CP_ERR_NULL (-1)        /* a required pointer is NULL                          */
@@ -64,14 +67,15 @@ typedef struct cp_states {
     uint32_t *ep_len;   /* [n] steps (= return) of the running episode             */
     int64_t n;          /* number of environments, 1 <= n <= 2^31 - 1              */
     uint32_t env_base;  /* global index of environment 0; env_base + n <= 2^32     */
-    int32_t variant;    /* CP_UNFUSED, CP_FUSED or CP_RESIDENT                     */
+    int32_t variant;    /* CP_UNFUSED, CP_FUSED, CP_RESIDENT or CP_CONCAT          */
     uint64_t seed;      /* set by cp_init: seed of the reset stream                */
     uint64_t t;         /* global step counter, advanced by cp_step / cp_rollout   */
     void *stream;       /* hipStream_t the calls are queued on                     */
     const uint16_t *policy_w; /* NULL = random actions; else CP_POLICY_WEIGHTS bf16
                                  bit patterns of the MLP policy (device memory,
                                  2-byte aligned), CP_RESIDENT only; see below      */
-    void *workspace;          /* CP_UNFUSED temporaries, >= cp_workspace_bytes()  */
+    void *workspace;          /* CP_UNFUSED / CP_CONCAT temporaries, at least
+                                 cp_workspace_bytes(); CP_CONCAT: 16-B aligned */
     size_t workspace_bytes;
     int64_t steps_per_launch; /* CP_RESIDENT rollouts: steps per kernel launch,
                                  the state going through HBM between launches
@@ -128,8 +132,8 @@ int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *reward, uin
  * steps_per_launch < 0 is CP_ERR_SIZE.                                      */
 int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
 
-/* Bytes of workspace CP_UNFUSED needs for n environments (0 for the other
- * variants, or for n out of range).                                         */
+/* Bytes of workspace CP_UNFUSED / CP_CONCAT need for n environments (0 for
+ * the other variants, or for n out of range).                               */
 size_t cp_workspace_bytes(int64_t n, int32_t variant);
 
 /* Message of the last failing call on this thread ("" if none).            */

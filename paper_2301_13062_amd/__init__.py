@@ -15,8 +15,8 @@ import os
 
 import torch
 
-CP_UNFUSED, CP_FUSED, CP_RESIDENT = 0, 1, 2
-VARIANTS = {"unfused": CP_UNFUSED, "fused": CP_FUSED, "resident": CP_RESIDENT}
+CP_UNFUSED, CP_FUSED, CP_RESIDENT, CP_CONCAT = 0, 1, 2, 3
+VARIANTS = {"unfused": CP_UNFUSED, "fused": CP_FUSED, "resident": CP_RESIDENT, "concat": CP_CONCAT}
 CP_OK, CP_ERR_NULL, CP_ERR_SIZE, CP_ERR_ALIGN, CP_ERR_RANGE, CP_ERR_HIP, CP_ERR_UNSUPPORTED = (
     0, -1, -2, -3, -4, -5, -6)
 CP_POLICY_WEIGHTS = 4480
@@ -99,8 +99,8 @@ class CartPoleStates:
         self.ep_index, self.ep_len = torch.zeros(self.n, **i32), torch.zeros(self.n, **i32)
         self.policy_w = policy_w
         self.workspace = workspace
-        if self.variant == CP_UNFUSED and workspace is None:
-            nbytes = cp_workspace_bytes(self.n, CP_UNFUSED)
+        if self.variant in (CP_UNFUSED, CP_CONCAT) and workspace is None:
+            nbytes = cp_workspace_bytes(self.n, self.variant)
             self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
         self.seed, self.t = 0, 0
         self.steps_per_launch = int(steps_per_launch)

@@ -42,7 +42,8 @@ int check_states(const cp_states *s) {
   if (!aligned4(s->x) || !aligned4(s->x_dot) || !aligned4(s->theta) || !aligned4(s->theta_dot) ||
       !aligned4(s->ep_index) || !aligned4(s->ep_len))
     return fail(CP_ERR_ALIGN, "state arrays must be 4-byte aligned");
-  if (s->variant != CP_UNFUSED && s->variant != CP_FUSED && s->variant != CP_RESIDENT)
+  if (s->variant != CP_UNFUSED && s->variant != CP_FUSED && s->variant != CP_RESIDENT &&
+      s->variant != CP_CONCAT)
     return fail(CP_ERR_UNSUPPORTED, "unknown variant %d", (int)s->variant);
   if (reinterpret_cast<uintptr_t>(s->policy_w) & 1u)
     return fail(CP_ERR_ALIGN, "policy weights must be 2-byte aligned");
@@ -56,15 +57,31 @@ int check_steps(const cp_states *s, uint64_t n_steps) {
   return CP_OK;
 }
 
+size_t workspace_need(int32_t variant, uint32_t n) {
+  if (variant == CP_UNFUSED) return cp::unfused_workspace_bytes(n);
+  if (variant == CP_CONCAT) return cp::concat_workspace_bytes(n);
+  return 0;
+}
+
 int check_workspace(const cp_states *s) {
-  if (s->variant != CP_UNFUSED) return CP_OK;
-  const size_t need = cp::unfused_workspace_bytes(uint32_t(s->n));
-  if (!s->workspace) return fail(CP_ERR_NULL, "CP_UNFUSED needs a workspace of %zu bytes", need);
-  if (!aligned4(s->workspace)) return fail(CP_ERR_ALIGN, "workspace must be 4-byte aligned");
+  const size_t need = workspace_need(s->variant, uint32_t(s->n));
+  if (need == 0) return CP_OK;
+  const char *name = s->variant == CP_UNFUSED ? "CP_UNFUSED" : "CP_CONCAT";
+  if (!s->workspace) return fail(CP_ERR_NULL, "%s needs a workspace of %zu bytes", name, need);
+  const uintptr_t align = s->variant == CP_CONCAT ? 16u : 4u;
+  if (reinterpret_cast<uintptr_t>(s->workspace) % align)
+    return fail(CP_ERR_ALIGN, "%s workspace must be %u-byte aligned", name, unsigned(align));
   if (s->workspace_bytes < need)
-    return fail(CP_ERR_SIZE, "workspace has %zu bytes, CP_UNFUSED needs %zu", s->workspace_bytes,
+    return fail(CP_ERR_SIZE, "workspace has %zu bytes, %s needs %zu", s->workspace_bytes, name,
                 need);
   return CP_OK;
+}
+
+// One step of the per-step levels (unfused, concatenated, fused).
+hipError_t launch_step(const cp_states *s, const cp::StepParams &p, hipStream_t st) {
+  if (s->variant == CP_UNFUSED) return cp::launch_unfused_step(p, s->workspace, st);
+  if (s->variant == CP_CONCAT) return cp::launch_concat_step(p, s->workspace, st);
+  return cp::launch_fused_step(p, st);
 }
 
 int hip_status(hipError_t e, const char *what) {
@@ -135,8 +152,7 @@ CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *rewa
     p.reward = reward;
     p.done = done;
     // Explicit actions under CP_RESIDENT: a single step is the fused step.
-    err = (s->variant == CP_UNFUSED) ? cp::launch_unfused_step(p, s->workspace, st)
-                                     : cp::launch_fused_step(p, st);
+    err = launch_step(s, p, st);
   }
   if (int e = hip_status(err, "cp_step launch")) return e;
   s->t += 1;
@@ -223,8 +239,7 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
         p.th = last ? s->theta : nullptr;
         p.thd = last ? s->theta_dot : nullptr;
       }
-      hipError_t err = (s->variant == CP_UNFUSED) ? cp::launch_unfused_step(p, s->workspace, st)
-                                                  : cp::launch_fused_step(p, st);
+      hipError_t err = launch_step(s, p, st);
       if (int e = hip_status(err, "cp_rollout launch")) {
         s->t += uint64_t(j);  // steps already queued stay counted
         return e;
@@ -244,8 +259,8 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
 }
 
 CP_API size_t cp_workspace_bytes(int64_t n, int32_t variant) {
-  if (variant != CP_UNFUSED || n < 1 || n > INT32_MAX) return 0;
-  return cp::unfused_workspace_bytes(uint32_t(n));
+  if (n < 1 || n > INT32_MAX) return 0;
+  return workspace_need(variant, uint32_t(n));
 }
 
 CP_API const char *cp_last_error(void) { return g_err; }

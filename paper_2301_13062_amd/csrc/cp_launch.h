@@ -63,6 +63,11 @@ hipError_t launch_episode_sums(const uint32_t *ep_index, const uint32_t *ep_len,
                                bool after, unsigned long long extra, unsigned long long *global,
                                hipStream_t stream);
 
+// Concatenated-state level: two kernels per step around an [n][4] array
+// (16 bytes per environment of workspace, 16-byte aligned).
+size_t concat_workspace_bytes(uint32_t n);
+hipError_t launch_concat_step(const StepParams &p, void *workspace, hipStream_t stream);
+
 // Unfused level: one kernel per primitive operation; temporaries live in the
 // caller's workspace.
 size_t unfused_workspace_bytes(uint32_t n);

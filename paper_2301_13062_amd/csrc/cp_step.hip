@@ -85,6 +85,56 @@ __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint3
   if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
 }
 
+// Concatenated-state level (the paper's baseline before its "no concat"
+// change, Sec. "Fusion via XLA Modification" and "Fusion via Memory Movement
+// Optimization"): the step is split at a concatenation of the four updated
+// state values into one [n][4] array that the second kernel reads back --
+// two launches and an extra 32 B per env-step through HBM, otherwise the
+// same arithmetic as the fused step.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+template <bool kExplicit>
+__global__ __launch_bounds__(kBlock) void k_concat_dynamics(StepParams p, f32x4 *cat) {
+  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+  uint32_t a = kExplicit ? 0u : action_bit_wave(p.kact, p.env_base + i, p.t);
+  if (i >= p.n) return;
+  if (kExplicit) a = uint32_t(p.actions[i] != 0);
+  const State o = dynamics(State{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]}, force_of(a));
+  cat[i] = f32x4{o.x, o.xd, o.th, o.thd};
+}
+
+__global__ __launch_bounds__(kBlock) void k_concat_finish(StepParams p, const f32x4 *cat) {
+  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+  if (i >= p.n) return;
+  const f32x4 v = cat[i];
+  State o{v[0], v[1], v[2], v[3]};
+  uint32_t len = p.ep_len[i] + 1u, ret = 0u;
+  const uint32_t d = terminated(o) ? 1u : 0u;
+  if (d) {
+    ret = len;
+    len = 0u;
+    const uint32_t k = p.ep_index[i] + 1u;
+    p.ep_index[i] = k;
+    o = reset_draw(p.krst, p.env_base + i, k);
+  }
+  p.x[i] = o.x;
+  p.xd[i] = o.xd;
+  p.th[i] = o.th;
+  p.thd[i] = o.thd;
+  p.ep_len[i] = len;
+  if (p.obs) {
+    __builtin_nontemporal_store(o.x, p.obs + i);
+    __builtin_nontemporal_store(o.xd, p.obs + p.n + i);
+    __builtin_nontemporal_store(o.th, p.obs + 2u * p.n + i);
+    __builtin_nontemporal_store(o.thd, p.obs + 3u * p.n + i);
+  }
+  if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + i);
+  if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + i);
+  if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + d;
+  if (p.total_reward) p.total_reward[i] = (p.first ? 0.0f : p.total_reward[i]) + 1.0f;
+  if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
+}
+
 template <bool kExplicit>
 __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
@@ -139,6 +189,19 @@ hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
     hipLaunchKernelGGL(k_fused_step<true>, grid_for(p.n), dim3(kBlock), 0, stream, p);
   else
     hipLaunchKernelGGL(k_fused_step<false>, grid_for(p.n), dim3(kBlock), 0, stream, p);
+  return hipGetLastError();
+}
+
+size_t concat_workspace_bytes(uint32_t n) { return size_t(n) * sizeof(f32x4); }
+
+hipError_t launch_concat_step(const StepParams &p, void *workspace, hipStream_t stream) {
+  f32x4 *cat = static_cast<f32x4 *>(workspace);
+  if (p.actions)
+    hipLaunchKernelGGL(k_concat_dynamics<true>, grid_for(p.n), dim3(kBlock), 0, stream, p, cat);
+  else
+    hipLaunchKernelGGL(k_concat_dynamics<false>, grid_for(p.n), dim3(kBlock), 0, stream, p, cat);
+  hipLaunchKernelGGL(k_concat_finish, grid_for(p.n), dim3(kBlock), 0, stream, p,
+                     static_cast<const f32x4 *>(cat));
   return hipGetLastError();
 }
 

@@ -66,7 +66,7 @@ def call_rollout(h, n, traj=None):
     ("theta", MIS, cp.CP_ERR_ALIGN),
     ("ep_index", A + 1, cp.CP_ERR_ALIGN),
     ("env_base", 2 ** 32 - 10, cp.CP_ERR_RANGE),
-    ("variant", 3, cp.CP_ERR_UNSUPPORTED),
+    ("variant", 4, cp.CP_ERR_UNSUPPORTED),
     ("variant", -1, cp.CP_ERR_UNSUPPORTED),
 ])
 def test_rejects_bad_state(fn, field, value, code):
@@ -120,6 +120,14 @@ def test_unfused_workspace_checks():
     assert call_rollout(h, 2) == cp.CP_ERR_SIZE
 
 
+def test_concat_workspace_checks():
+    need = cp.cp_workspace_bytes(1000, cp.CP_CONCAT)
+    assert need == 1000 * 16
+    assert call_step(handle(variant=cp.CP_CONCAT)) == cp.CP_ERR_NULL
+    assert call_step(handle(variant=cp.CP_CONCAT, workspace=A + 4, workspace_bytes=need)) == cp.CP_ERR_ALIGN
+    assert call_rollout(handle(variant=cp.CP_CONCAT, workspace=A, workspace_bytes=need - 16), 2) == cp.CP_ERR_SIZE
+
+
 def test_policy_weights_alignment():
     h = handle(variant=cp.CP_RESIDENT, policy_w=A + 1)
     assert call_rollout(h, 2) == cp.CP_ERR_ALIGN
@@ -127,7 +135,7 @@ def test_policy_weights_alignment():
 
 
 def test_policy_needs_resident_variant():
-    for v in (cp.CP_FUSED, cp.CP_UNFUSED):
+    for v in (cp.CP_FUSED, cp.CP_UNFUSED, cp.CP_CONCAT):
         h = handle(variant=v, policy_w=A, workspace=A,
                    workspace_bytes=cp.cp_workspace_bytes(1000, cp.CP_UNFUSED))
         assert call_step(h) == cp.CP_ERR_UNSUPPORTED

@@ -20,8 +20,9 @@ from paper_2301_13062_amd import synth
 
 pytestmark = pytest.mark.gpu
 
-ALL = [cp.CP_UNFUSED, cp.CP_FUSED, cp.CP_RESIDENT]
-NAMES = {cp.CP_UNFUSED: "unfused", cp.CP_FUSED: "fused", cp.CP_RESIDENT: "resident"}
+ALL = [cp.CP_UNFUSED, cp.CP_CONCAT, cp.CP_FUSED, cp.CP_RESIDENT]
+NAMES = {cp.CP_UNFUSED: "unfused", cp.CP_CONCAT: "concat", cp.CP_FUSED: "fused",
+         cp.CP_RESIDENT: "resident"}
 STEP_ABS, STEP_REL = 1e-6, 1e-5
 ROLL_MATCH, ROLL_ABS = 0.999, 1e-3
 
@@ -148,7 +149,7 @@ def test_fusion_levels_bit_identical(gpu):
     n, T = 5003, 101  # spans two 64-step action blocks and a ragged wave
     res = {v: run(v, n, T, seed=3, act_seed=4) for v in ALL}
     ref_s, ref_t = res[cp.CP_FUSED]
-    for v in (cp.CP_UNFUSED, cp.CP_RESIDENT):
+    for v in (cp.CP_UNFUSED, cp.CP_CONCAT, cp.CP_RESIDENT):
         s, tr = res[v]
         for a, b in zip(gpu_state(s), gpu_state(ref_s)):
             assert np.array_equal(a, b), NAMES[v]
@@ -191,7 +192,8 @@ def _oracle_65536x1000():
     return _ORACLE_CACHE["c2"]
 
 
-@pytest.mark.parametrize("variant", [cp.CP_UNFUSED, cp.CP_FUSED], ids=lambda v: NAMES[v])
+@pytest.mark.parametrize("variant", [cp.CP_UNFUSED, cp.CP_CONCAT, cp.CP_FUSED],
+                         ids=lambda v: NAMES[v])
 def test_rollout_65536x1000_one_step_per_launch(gpu, variant):
     n, T = 65536, 1000
     s, tr = run(variant, n, T, seed=0, obs=False, reward=False)
@@ -344,14 +346,14 @@ def test_explicit_actions_under_resident_equal_fused(gpu):
     n, T = 2000, 25
     acts = torch.from_numpy(synth.actions(T, n, seed=5)).cuda()
     outs = {}
-    for v in (cp.CP_FUSED, cp.CP_RESIDENT, cp.CP_UNFUSED):
+    for v in (cp.CP_FUSED, cp.CP_RESIDENT, cp.CP_UNFUSED, cp.CP_CONCAT):
         s = cp.CartPoleStates(n, variant=v)
         cp.cp_init(s, 2)
         for j in range(T):
             cp.cp_step(s, acts[j])
         torch.cuda.synchronize()
         outs[v] = gpu_state(s)
-    for v in (cp.CP_RESIDENT, cp.CP_UNFUSED):
+    for v in (cp.CP_RESIDENT, cp.CP_UNFUSED, cp.CP_CONCAT):
         assert all(np.array_equal(x, y) for x, y in zip(outs[v], outs[cp.CP_FUSED]))
     o = O.OracleState(n)
     O.init(o, 2)
