@@ -16,7 +16,8 @@ Also measured in the same run (extra keys of the same JSON line):
   roofline  HBM roofline of the fused step kernel: algorithmic bytes per
             launch over the mean launch duration (HIP events around the
             timed region of back-to-back launches, divided by the launches);
-  cpu_baseline  the CPU oracle on the host cores (one thread).
+  cpu_baseline  the CPU oracle on the host cores (one thread), and a
+            small-batch sweep against the resident kernel (crossover).
 
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick]
 """
@@ -65,8 +66,8 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 COUNTER_SOURCES = ["paper_2301_13062_amd/csrc/cp_step.hip", "paper_2301_13062_amd/csrc/cp_device.h",
                    "paper_2301_13062_amd/csrc/cp_launch.h", "paper_2301_13062_amd/csrc/cp_resident.h",
                    "paper_2301_13062_amd/csrc/cp_capi.hip", "paper_2301_13062_amd/build.py"]
-COUNTERS = {"sources_sha256_16": "5ced128ceae1e378",
-            "fused_step_65536": {"fetch_kib": 776.4, "write_kib": 2702.2},
+COUNTERS = {"sources_sha256_16": "dc53fb4f32b16661",
+            "fused_step_65536": {"fetch_kib": 806.5, "write_kib": 2702.2},
             "read_factor": 1.99995, "write_factor": 1.0}
 
 
@@ -263,6 +264,49 @@ def _policy(cp):
                          "flops_per_env_step": POLICY_FLOPS}}
 
 
+CROSSOVER_N = (1, 4, 16, 64, 256, 1024, 4096)
+
+
+def _oracle_rate(n, T, workers):
+    """Oracle env-steps/s on n environments x T steps, the environments split
+    over `workers` threads (independent ranges; the C oracle releases the
+    GIL through ctypes)."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
+    import oracle as O
+
+    parts = [p for p in np.array_split(np.arange(n, dtype=np.uint32), min(workers, n)) if len(p)]
+    states = []
+    for ids in parts:
+        o = O.OracleState(len(ids), ids)
+        O.init(o, 0)
+        states.append(o)
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=len(states)) as ex:
+        list(ex.map(lambda o: O.rollout(o, T), states))
+    return n * T / (time.perf_counter() - t0)
+
+
+def crossover(cp, T=1000):
+    """Small-batch sweep (the paper's CPU/GPU comparison): the register-
+    resident kernel against the CPU oracle on one thread and on the host's
+    cores, N environments x T steps, random actions."""
+    workers = min(16, os.cpu_count() or 1)
+    rows = {}
+    for n in CROSSOVER_N:
+        s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+        cp.cp_init(s, 0)
+        cp.cp_rollout(s, T, 0, None)
+        wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, None), reps=5)
+        rows[str(n)] = {"gpu": n * T * 5 / (wall * 1e-3), "cpu_1": _oracle_rate(n, T, 1),
+                        "cpu_all": _oracle_rate(n, T, workers)}
+    faster = [int(k) for k, r in rows.items() if r["gpu"] > r["cpu_all"]]
+    return {"steps": T, "cpu_workers": workers, "env_steps_per_s": rows,
+            "gpu_faster_from_n": min(faster) if faster else None}
+
+
 def cpu_baseline():
     import oracle as O
 
@@ -333,6 +377,8 @@ def main():
         line["unroll"] = bench_unroll(cp)
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline()
+        if not args.quick:
+            line["cpu_baseline"]["crossover"] = crossover(cp)
     print(json.dumps(line))
 
 

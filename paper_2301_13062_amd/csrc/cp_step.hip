@@ -22,6 +22,10 @@ namespace cp {
 namespace {
 
 constexpr int kBlock = 256;
+// Batches below this size take the latency-oriented fused step (kEager);
+// from it on the bandwidth-oriented one, which touches the episode index
+// only on termination.
+constexpr uint32_t kEagerMaxEnvs = 1u << 21;
 
 
 __global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *__restrict__ xd,
@@ -40,31 +44,11 @@ __global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *_
   ep_len[i] = 0u;
 }
 
-// One environment's step after its action is known: dynamics, termination,
-// reset.  len is the running episode length (updated); d / ret report the
-// termination and the finished episode's return.
-__device__ __forceinline__ State advance(const StepParams &p, uint32_t i, State s, uint32_t a,
-                                         uint32_t &len, uint32_t &d, uint32_t &ret) {
-  State o = dynamics(s, force_of(a));
-  len += 1u;
-  d = terminated(o) ? 1u : 0u;
-  ret = 0u;
-  if (d) {
-    ret = len;
-    len = 0u;
-    const uint32_t k = p.ep_index[i] + 1u;
-    p.ep_index[i] = k;
-    o = reset_draw(p.krst, p.env_base + i, k);
-  }
-  return o;
-}
-
-template <bool kExplicit>
-__device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
-  const State s{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
-  if (kExplicit) a = uint32_t(p.actions[i] != 0);
-  uint32_t len = p.ep_len[i], d, ret;
-  const State o = advance(p, i, s, a, len, d, ret);
+// Stores of one environment's step: the state (unless the trajectory's obs
+// plane holds it), the running episode length, the step outputs and the
+// rollout accumulators.
+__device__ __forceinline__ void store_step(const StepParams &p, uint32_t i, const State &o,
+                                           uint32_t len, uint32_t d, uint32_t ret) {
   if (p.x) {
     p.x[i] = o.x;
     p.xd[i] = o.xd;
@@ -83,6 +67,37 @@ __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint3
   if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + d;
   if (p.total_reward) p.total_reward[i] = (p.first ? 0.0f : p.total_reward[i]) + 1.0f;
   if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
+}
+
+// One environment of the fused step.  kEager (small batches, where a step
+// is latency-bound): the episode index is loaded with the state and the
+// next start state drawn while the dynamics run, instead of a second memory
+// round trip and the draw after the termination test; the episode index is
+// still written only on termination.
+template <bool kExplicit, bool kEager>
+__device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
+  const uint32_t env = p.env_base + i;
+  const State s{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
+  if (kExplicit) a = uint32_t(p.actions[i] != 0);
+  uint32_t len = p.ep_len[i] + 1u, ret = 0u, k = 0u;
+  State r{0.f, 0.f, 0.f, 0.f};
+  if (kEager) {
+    k = p.ep_index[i] + 1u;
+    r = reset_draw(p.krst, env, k);
+  }
+  State o = dynamics(s, force_of(a));
+  const uint32_t d = terminated(o) ? 1u : 0u;
+  if (d) {
+    ret = len;
+    len = 0u;
+    if (!kEager) {
+      k = p.ep_index[i] + 1u;
+      r = reset_draw(p.krst, env, k);
+    }
+    p.ep_index[i] = k;
+    o = r;
+  }
+  store_step(p, i, o, len, d, ret);
 }
 
 // Concatenated-state level (the paper's baseline before its "no concat"
@@ -117,30 +132,15 @@ __global__ __launch_bounds__(kBlock) void k_concat_finish(StepParams p, const f3
     p.ep_index[i] = k;
     o = reset_draw(p.krst, p.env_base + i, k);
   }
-  p.x[i] = o.x;
-  p.xd[i] = o.xd;
-  p.th[i] = o.th;
-  p.thd[i] = o.thd;
-  p.ep_len[i] = len;
-  if (p.obs) {
-    __builtin_nontemporal_store(o.x, p.obs + i);
-    __builtin_nontemporal_store(o.xd, p.obs + p.n + i);
-    __builtin_nontemporal_store(o.th, p.obs + 2u * p.n + i);
-    __builtin_nontemporal_store(o.thd, p.obs + 3u * p.n + i);
-  }
-  if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + i);
-  if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + i);
-  if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + d;
-  if (p.total_reward) p.total_reward[i] = (p.first ? 0.0f : p.total_reward[i]) + 1.0f;
-  if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
+  store_step(p, i, o, len, d, ret);
 }
 
-template <bool kExplicit>
+template <bool kExplicit, bool kEager>
 __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
   // random actions: one block per wave, before any lane leaves
   const uint32_t a = kExplicit ? 0u : action_bit_wave(p.kact, p.env_base + i, p.t);
-  if (i < p.n) fused_one<kExplicit>(p, i, a);
+  if (i < p.n) fused_one<kExplicit, kEager>(p, i, a);
 }
 
 template <bool kTraj>
@@ -185,10 +185,15 @@ hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_
 }
 
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
-  if (p.actions)
-    hipLaunchKernelGGL(k_fused_step<true>, grid_for(p.n), dim3(kBlock), 0, stream, p);
-  else
-    hipLaunchKernelGGL(k_fused_step<false>, grid_for(p.n), dim3(kBlock), 0, stream, p);
+  const dim3 g = grid_for(p.n), b(kBlock);
+  const bool eager = p.n < kEagerMaxEnvs;
+  if (p.actions) {
+    if (eager) hipLaunchKernelGGL((k_fused_step<true, true>), g, b, 0, stream, p);
+    else hipLaunchKernelGGL((k_fused_step<true, false>), g, b, 0, stream, p);
+  } else {
+    if (eager) hipLaunchKernelGGL((k_fused_step<false, true>), g, b, 0, stream, p);
+    else hipLaunchKernelGGL((k_fused_step<false, false>), g, b, 0, stream, p);
+  }
   return hipGetLastError();
 }
 
