@@ -88,7 +88,7 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
-    ap.add_argument("--warmup", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--quick", action="store_true", help="headline only, no extra configs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", choices=["resident_1024x200", "resident_1048576x1000",
@@ -123,16 +123,25 @@ def bench_headline(cp, K, W):
 
     n = 65536
     out = {}
-    for name, variant in (("fused", cp.CP_FUSED), ("concat", cp.CP_CONCAT),
-                          ("unfused", cp.CP_UNFUSED)):
-        s = cp.CartPoleStates(n, variant=variant)
+    for name, variant, graphs in (("fused", cp.CP_FUSED, True),
+                                  ("fused_direct", cp.CP_FUSED, False),
+                                  ("concat", cp.CP_CONCAT, False),
+                                  ("unfused", cp.CP_UNFUSED, False)):
+        s = cp.CartPoleStates(n, variant=variant, graphs=graphs)
         cp.cp_init(s, 0)
-        warm = cp.Trajectory(n, W, stats=False, totals=False)
-        cp.cp_rollout(s, W, 0, warm)
-        del warm
         tr = cp.Trajectory(n, K, stats=False, totals=False)
+        # W warm-up steps as calls of the timed call's shape (K steps into
+        # the same buffers; with graphs, the first such call is recorded
+        # and the second builds the graph that the timed call replays)
+        left = W
+        while left > 0:
+            steps = min(K, left)
+            cp.cp_rollout(s, steps, 0, tr if steps == K else None)
+            left -= steps
         # the library launches the K step kernels back to back on torch's
-        # current stream; HIP events bracket the whole timed region
+        # current stream (fused: replayed from the HIP graph built during
+        # the warm-up; fused_direct: one host launch per step); HIP
+        # events bracket the whole timed region
         wall, ev = timed(lambda: cp.cp_rollout(s, K, 0, tr))
         out[name] = {"wall_ms": wall, "event_ms": ev, "env_steps_per_s": n * K / (wall * 1e-3),
                      "us_per_step": wall * 1e3 / K, "event_us_per_step": ev * 1e3 / K}
@@ -371,6 +380,9 @@ def main():
         "concat": {"env_steps_per_s": head["concat"]["env_steps_per_s"],
                    "us_per_step": head["concat"]["us_per_step"]},
         "no_concat_speedup": fused["env_steps_per_s"] / head["concat"]["env_steps_per_s"],
+        "fused_direct": {"env_steps_per_s": head["fused_direct"]["env_steps_per_s"],
+                         "us_per_step": head["fused_direct"]["us_per_step"]},
+        "graph_speedup": fused["env_steps_per_s"] / head["fused_direct"]["env_steps_per_s"],
     }
     if not args.quick:
         line["configs"] = bench_configs(cp)

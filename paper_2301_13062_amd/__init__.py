@@ -89,7 +89,7 @@ class CartPoleStates:
     """
 
     def __init__(self, n, variant=CP_FUSED, device="cuda", env_base=0, policy_w=None,
-                 workspace=None, steps_per_launch=0):
+                 workspace=None, steps_per_launch=0, graphs=True):
         self.n, self.env_base = int(n), int(env_base)
         self.variant = VARIANTS.get(variant, variant)
         f32 = dict(dtype=torch.float32, device=device)
@@ -99,7 +99,11 @@ class CartPoleStates:
         self.ep_index, self.ep_len = torch.zeros(self.n, **i32), torch.zeros(self.n, **i32)
         self.policy_w = policy_w
         self.workspace = workspace
-        if self.variant in (CP_UNFUSED, CP_CONCAT) and workspace is None:
+        # CP_UNFUSED and CP_CONCAT need a workspace; CP_FUSED takes one to
+        # replay per-step rollouts from HIP graphs (graphs=False: one launch
+        # per step from the host).
+        needs = self.variant in (CP_UNFUSED, CP_CONCAT) or (self.variant == CP_FUSED and graphs)
+        if needs and workspace is None:
             nbytes = cp_workspace_bytes(self.n, self.variant)
             self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=device)
         self.seed, self.t = 0, 0

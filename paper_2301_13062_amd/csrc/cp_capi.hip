@@ -14,8 +14,6 @@ namespace {
 
 thread_local char g_err[512];
 
-constexpr size_t kObsStateMinEnvs = size_t(1) << 21;
-
 int fail(int code, const char *fmt, ...) {
   va_list ap;
   va_start(ap, fmt);
@@ -60,15 +58,21 @@ int check_steps(const cp_states *s, uint64_t n_steps) {
 size_t workspace_need(int32_t variant, uint32_t n) {
   if (variant == CP_UNFUSED) return cp::unfused_workspace_bytes(n);
   if (variant == CP_CONCAT) return cp::concat_workspace_bytes(n);
+  if (variant == CP_FUSED) return cp::fused_workspace_bytes(n);
   return 0;
 }
 
+// CP_UNFUSED and CP_CONCAT need their workspace; for CP_FUSED it is
+// optional (it enables graph replay of repeated rollouts).
 int check_workspace(const cp_states *s) {
   const size_t need = workspace_need(s->variant, uint32_t(s->n));
   if (need == 0) return CP_OK;
-  const char *name = s->variant == CP_UNFUSED ? "CP_UNFUSED" : "CP_CONCAT";
+  if (s->variant == CP_FUSED && !s->workspace) return CP_OK;
+  const char *name = s->variant == CP_UNFUSED ? "CP_UNFUSED"
+                     : s->variant == CP_CONCAT ? "CP_CONCAT"
+                                               : "CP_FUSED";
   if (!s->workspace) return fail(CP_ERR_NULL, "%s needs a workspace of %zu bytes", name, need);
-  const uintptr_t align = s->variant == CP_CONCAT ? 16u : 4u;
+  const uintptr_t align = s->variant == CP_UNFUSED ? 4u : 16u;
   if (reinterpret_cast<uintptr_t>(s->workspace) % align)
     return fail(CP_ERR_ALIGN, "%s workspace must be %u-byte aligned", name, unsigned(align));
   if (s->workspace_bytes < need)
@@ -218,8 +222,22 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
     // Used for batches whose state does not stay in the caches between
     // launches (below that size the state arrays are re-read from cache,
     // while the trajectory is written past it).
-    const bool obs_state = s->variant == CP_FUSED && tr.obs && n >= kObsStateMinEnvs;
-    for (int64_t j = 0; j < n_steps; ++j) {
+    const bool obs_state = s->variant == CP_FUSED && tr.obs && n >= cp::kObsStateMinEnvs;
+    // With a CP_FUSED workspace, a rollout that repeats an earlier call's
+    // arrays, outputs and length is replayed from a HIP graph.
+    bool replayed = false;
+    if (s->variant == CP_FUSED && s->workspace && !obs_state &&
+        n_steps <= int64_t(cp::kGraphMaxSteps)) {
+      p.t = uint32_t(s->t);
+      p.obs = tr.obs;
+      p.reward = tr.reward;
+      p.done = tr.done;
+      if (int e = hip_status(cp::launch_fused_graph(p, uint32_t(n_steps), s->workspace, st,
+                                                    &replayed),
+                             "cp_rollout graph"))
+        return e;
+    }
+    for (int64_t j = 0; j < n_steps && !replayed; ++j) {
       p.t = uint32_t(s->t + uint64_t(j));
       p.first = j == 0;
       p.obs = tr.obs ? tr.obs + size_t(j) * 4u * n : nullptr;
@@ -239,7 +257,7 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
         p.th = last ? s->theta : nullptr;
         p.thd = last ? s->theta_dot : nullptr;
       }
-      hipError_t err = launch_step(s, p, st);
+      const hipError_t err = launch_step(s, p, st);
       if (int e = hip_status(err, "cp_rollout launch")) {
         s->t += uint64_t(j);  // steps already queued stay counted
         return e;

@@ -48,10 +48,40 @@ struct RolloutParams {
   uint32_t first;            // 1: per-env statistics start at this launch
 };
 
+// Batches from this size on with an obs trajectory read each step's state
+// from the previous step's obs plane; below it a step is latency-bound.
+constexpr uint32_t kObsStateMinEnvs = 1u << 21;
+
+// Graph replay of fused rollouts (latency-bound batches, random actions).
+// The per-call values a replay needs -- the action key and the first step
+// index -- sit in a descriptor at the start of the workspace; after it, the
+// actions of kWordRows consecutive steps as one 64-bit word per wave of 64
+// environments and step.
+struct GraphDesc {
+  U2 kact;
+  uint32_t t;
+};
+constexpr size_t kGraphDescBytes = 256;
+constexpr uint32_t kWordRows = 128u;
+// Rollout lengths replayed from graphs.
+constexpr uint32_t kGraphMinSteps = 16u, kGraphMaxSteps = 8192u;
+inline size_t fused_workspace_bytes(uint32_t n) {
+  if (n >= kObsStateMinEnvs) return 0;
+  return kGraphDescBytes + 8u * size_t(kWordRows) * ((size_t(n) + 63u) / 64u);
+}
+
 hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_index,
                        uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst,
                        hipStream_t stream);
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream);
+// A fused rollout of T steps with random actions from one cached HIP graph,
+// for a rollout whose arrays, outputs and length repeat those of an earlier
+// call (base: step 0's parameters, obs/reward/done at row 0; its step
+// index and action key are per call).  The first call of a kind records it
+// and launches nothing, as do calls during stream capture or with the
+// graph cache full: *used says whether the steps were launched.
+hipError_t launch_fused_graph(const StepParams &base, uint32_t T, void *workspace,
+                              hipStream_t stream, bool *used);
 // Register-resident rollout; with p.policy_w set the MLP policy chooses the
 // actions (launch_resident_policy), otherwise the random action stream.
 hipError_t launch_resident(const RolloutParams &p, hipStream_t stream);

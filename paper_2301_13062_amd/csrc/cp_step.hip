@@ -14,6 +14,9 @@
 // Resident rollout with random actions (paper Sec. "Fusion via Unroll" and
 // Sec. "Comparison with CUDA implementation": all steps in one kernel): the
 // loop itself is shared with the MLP-policy kernel (cp_resident.h).
+#include <mutex>
+#include <vector>
+
 #include "cp_launch.h"
 #include "cp_resident.h"
 
@@ -25,7 +28,29 @@ constexpr int kBlock = 256;
 // Batches below this size take the latency-oriented fused step (kEager);
 // from it on the bandwidth-oriented one, which touches the episode index
 // only on termination.
-constexpr uint32_t kEagerMaxEnvs = 1u << 21;
+constexpr uint32_t kEagerMaxEnvs = kObsStateMinEnvs;
+
+// Accesses through pointers that the compiler cannot place in global memory
+// by itself (pointers loaded from memory rather than passed as kernel
+// arguments) are typed as global, so that they compile to global rather
+// than flat instructions.
+template <class T>
+using global_ptr = __attribute__((address_space(1))) T *;
+
+template <class T>
+__device__ __forceinline__ void st_global(T *base, size_t i, T v) {
+  ((global_ptr<T>)base)[i] = v;
+}
+
+template <class T>
+__device__ __forceinline__ void st_global_nt(T *base, size_t i, T v) {
+  __builtin_nontemporal_store(v, (global_ptr<T>)base + i);
+}
+
+template <class T>
+__device__ __forceinline__ T ld_global(const T *base, size_t i) {
+  return ((global_ptr<const T>)base)[i];
+}
 
 
 __global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *__restrict__ xd,
@@ -50,39 +75,41 @@ __global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *_
 __device__ __forceinline__ void store_step(const StepParams &p, uint32_t i, const State &o,
                                            uint32_t len, uint32_t d, uint32_t ret) {
   if (p.x) {
-    p.x[i] = o.x;
-    p.xd[i] = o.xd;
-    p.th[i] = o.th;
-    p.thd[i] = o.thd;
+    st_global(p.x, i, o.x);
+    st_global(p.xd, i, o.xd);
+    st_global(p.th, i, o.th);
+    st_global(p.thd, i, o.thd);
   }
-  p.ep_len[i] = len;
+  st_global(p.ep_len, i, len);
   if (p.obs) {
-    __builtin_nontemporal_store(o.x, p.obs + i);
-    __builtin_nontemporal_store(o.xd, p.obs + p.n + i);
-    __builtin_nontemporal_store(o.th, p.obs + 2u * p.n + i);
-    __builtin_nontemporal_store(o.thd, p.obs + 3u * p.n + i);
+    st_global_nt(p.obs, i, o.x);
+    st_global_nt(p.obs, p.n + i, o.xd);
+    st_global_nt(p.obs, 2u * p.n + i, o.th);
+    st_global_nt(p.obs, 3u * p.n + i, o.thd);
   }
-  if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + i);
-  if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + i);
-  if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + d;
-  if (p.total_reward) p.total_reward[i] = (p.first ? 0.0f : p.total_reward[i]) + 1.0f;
-  if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
+  if (p.reward) st_global_nt(p.reward, i, 1.0f);
+  if (p.done) st_global_nt(p.done, i, uint8_t(d));
+  if (p.done_count)
+    st_global(p.done_count, i, (p.first ? 0u : ld_global(p.done_count, i)) + d);
+  if (p.total_reward)
+    st_global(p.total_reward, i, (p.first ? 0.0f : ld_global(p.total_reward, i)) + 1.0f);
+  if (p.ret_sum) st_global(p.ret_sum, i, (p.first ? 0u : ld_global(p.ret_sum, i)) + ret);
 }
 
-// One environment of the fused step.  kEager (small batches, where a step
-// is latency-bound): the episode index is loaded with the state and the
-// next start state drawn while the dynamics run, instead of a second memory
-// round trip and the draw after the termination test; the episode index is
-// still written only on termination.
-template <bool kExplicit, bool kEager>
-__device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
+// The fused step of one environment after its loads: s, its running
+// episode length and (kEager) its episode index k0.  kEager (small batches,
+// where a step is latency-bound): the episode index was loaded with the
+// state and the next start state is drawn while the dynamics run, instead of
+// a second memory round trip and the draw after the termination test; the
+// episode index is still written only on termination.
+template <bool kEager>
+__device__ __forceinline__ void fused_rest(const StepParams &p, uint32_t i, uint32_t a,
+                                           const State &s, uint32_t len0, uint32_t k0) {
   const uint32_t env = p.env_base + i;
-  const State s{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
-  if (kExplicit) a = uint32_t(p.actions[i] != 0);
-  uint32_t len = p.ep_len[i] + 1u, ret = 0u, k = 0u;
+  uint32_t len = len0 + 1u, ret = 0u, k = 0u;
   State r{0.f, 0.f, 0.f, 0.f};
   if (kEager) {
-    k = p.ep_index[i] + 1u;
+    k = k0 + 1u;
     r = reset_draw(p.krst, env, k);
   }
   State o = dynamics(s, force_of(a));
@@ -98,6 +125,13 @@ __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint3
     o = r;
   }
   store_step(p, i, o, len, d, ret);
+}
+
+template <bool kExplicit, bool kEager>
+__device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
+  const State s{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
+  if (kExplicit) a = uint32_t(p.actions[i] != 0);
+  fused_rest<kEager>(p, i, a, s, p.ep_len[i], kEager ? p.ep_index[i] : 0u);
 }
 
 // Concatenated-state level (the paper's baseline before its "no concat"
@@ -141,6 +175,161 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   // random actions: one block per wave, before any lane leaves
   const uint32_t a = kExplicit ? 0u : action_bit_wave(p.kact, p.env_base + i, p.t);
   if (i < p.n) fused_one<kExplicit, kEager>(p, i, a);
+}
+
+// Graph replay of fused rollouts.  Launched one by one, a latency-bound
+// step costs the host more than the GPU; a graph hands the GPU all steps of
+// a rollout at once.  Its launches cannot change their arguments from
+// replay to replay, so the two things that change from call to call with
+// the same arrays and outputs -- the step index and the action key -- reach
+// the steps through the actions: a word kernel at the head of every
+// kWordRows steps reads them from the workspace descriptor and writes each
+// wave's action word per step, which the step loads with its state.
+
+// The actions of one wave of 64 consecutive environments starting at env0
+// as one word (bit L: lane L), from the one or two 64-environment blocks it
+// covers.
+__device__ __forceinline__ unsigned long long wave_word(U2 key, uint32_t env0, uint32_t t) {
+  const uint32_t g0 = env0 >> 6, off = env0 & 63u;
+  const U2 b0 = threefry2x32(key.a, key.b, g0, t);
+  const unsigned long long w0 = (static_cast<unsigned long long>(b0.b) << 32) | b0.a;
+  if (off == 0u) return w0;
+  const U2 b1 = threefry2x32(key.a, key.b, g0 + 1u, t);
+  const unsigned long long w1 = (static_cast<unsigned long long>(b1.b) << 32) | b1.a;
+  return (w0 >> off) | (w1 << (64u - off));
+}
+
+// words[c][w] = actions of wave w at step d->t + t_off + c, for c < rows.
+__global__ __launch_bounds__(kBlock) void k_words(const GraphDesc *__restrict__ d,
+                                                  unsigned long long *__restrict__ words,
+                                                  uint32_t n, uint32_t env_base, uint32_t t_off,
+                                                  uint32_t rows) {
+  const uint32_t waves = (n + 63u) / 64u;
+  const uint32_t idx = blockIdx.x * kBlock + threadIdx.x;
+  if (idx >= rows * waves) return;
+  const uint32_t c = idx / waves, w = idx - c * waves;
+  words[idx] = wave_word(d->kact, env_base + 64u * w, d->t + t_off + c);
+}
+
+// The latency-ordered fused step with the wave's actions from its word in
+// `row`.  Lanes past the batch load the last environment: no branch around
+// the loads, so nothing waits for them before the word is loaded.
+__global__ __launch_bounds__(kBlock) void k_fused_step_words(
+    StepParams p, const unsigned long long *__restrict__ row) {
+  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+  const bool valid = i < p.n;
+  const uint32_t ic = valid ? i : p.n - 1u;
+  const State s{p.xi[ic], p.xdi[ic], p.thi[ic], p.thdi[ic]};
+  const uint32_t len0 = p.ep_len[ic], k0 = p.ep_index[ic];
+  const unsigned long long word = row[__builtin_amdgcn_readfirstlane(ic >> 6)];
+  const uint32_t a = uint32_t(word >> (threadIdx.x & 63u)) & 1u;
+  if (valid) fused_rest<true>(p, i, a, s, len0, k0);
+}
+
+__global__ __launch_bounds__(64) void k_graph_set(GraphDesc v, GraphDesc *d) {
+  if (threadIdx.x == 0) *d = v;
+}
+
+// What a rollout graph is built from: step 0's parameters (obs/reward/done
+// at row 0; step index and action key unused), the length and the
+// workspace.
+struct RolloutKey {
+  int device;
+  StepParams base;
+  uint32_t T;
+  void *workspace;
+  bool operator==(const RolloutKey &o) const {
+    const StepParams &a = base, &b = o.base;
+    return device == o.device && T == o.T && workspace == o.workspace && a.xi == b.xi &&
+           a.xdi == b.xdi && a.thi == b.thi && a.thdi == b.thdi && a.x == b.x && a.xd == b.xd &&
+           a.th == b.th && a.thd == b.thd && a.ep_index == b.ep_index && a.ep_len == b.ep_len &&
+           a.n == b.n && a.env_base == b.env_base && a.krst.a == b.krst.a &&
+           a.krst.b == b.krst.b && a.obs == b.obs && a.reward == b.reward && a.done == b.done &&
+           a.done_count == b.done_count && a.total_reward == b.total_reward &&
+           a.ret_sum == b.ret_sum;
+  }
+};
+
+// Graphs are kept for the life of the process (a replay may still be in
+// flight when a later call looks them up); past kMaxGraphs new kinds of
+// rollout run launch by launch.
+constexpr size_t kMaxGraphs = 32, kMaxSeen = 64;
+
+struct RolloutGraph {
+  RolloutKey key;
+  hipGraphExec_t exec;
+};
+
+std::mutex g_graph_mutex;
+std::vector<RolloutGraph> g_graphs;
+std::vector<RolloutKey> g_seen;  // kinds met once, oldest first
+
+hipError_t build_rollout_graph(const RolloutKey &k, hipGraphExec_t *out) {
+  hipGraph_t g = nullptr;
+  hipError_t e = hipGraphCreate(&g, 0);
+  if (e != hipSuccess) return e;
+  const GraphDesc *desc = static_cast<const GraphDesc *>(k.workspace);
+  unsigned long long *table = reinterpret_cast<unsigned long long *>(
+      static_cast<char *>(k.workspace) + kGraphDescBytes);
+  uint32_t n = k.base.n, env_base = k.base.env_base;
+  const uint32_t waves = (n + 63u) / 64u;
+  hipGraphNode_t prev = nullptr;
+  auto add = [&](void *func, dim3 grid, void **args) {
+    hipKernelNodeParams kp{};
+    kp.func = func;
+    kp.gridDim = grid;
+    kp.blockDim = dim3(kBlock);
+    kp.kernelParams = args;
+    hipGraphNode_t node = nullptr;
+    e = hipGraphAddKernelNode(&node, g, prev ? &prev : nullptr, prev ? 1 : 0, &kp);
+    prev = node;
+  };
+  for (uint32_t j = 0; j < k.T && e == hipSuccess; ++j) {
+    const uint32_t c = j % kWordRows;
+    if (c == 0u) {
+      uint32_t t_off = j, rows = k.T - j < kWordRows ? k.T - j : kWordRows;
+      void *args[] = {&desc, &table, &n, &env_base, &t_off, &rows};
+      add(reinterpret_cast<void *>(&k_words), dim3((rows * waves + kBlock - 1) / kBlock), args);
+      if (e != hipSuccess) break;
+    }
+    StepParams p = k.base;
+    p.first = j == 0u;
+    if (p.obs) p.obs += size_t(j) * 4u * n;
+    if (p.reward) p.reward += size_t(j) * n;
+    if (p.done) p.done += size_t(j) * n;
+    const unsigned long long *row = table + size_t(c) * waves;
+    void *args[] = {&p, &row};
+    add(reinterpret_cast<void *>(&k_fused_step_words), dim3((n + kBlock - 1) / kBlock), args);
+  }
+  if (e == hipSuccess) e = hipGraphInstantiate(out, g, nullptr, nullptr, 0);
+  hipGraphDestroy(g);
+  return e;
+}
+
+// The graph for this kind of rollout: built on its second call (the first
+// is only recorded), or nullptr.
+hipError_t rollout_graph(const RolloutKey &k, hipGraphExec_t *out) {
+  *out = nullptr;
+  std::lock_guard<std::mutex> lock(g_graph_mutex);
+  for (const RolloutGraph &rg : g_graphs)
+    if (rg.key == k) {
+      *out = rg.exec;
+      return hipSuccess;
+    }
+  if (g_graphs.size() >= kMaxGraphs) return hipSuccess;
+  bool seen = false;
+  for (const RolloutKey &s : g_seen) seen = seen || s == k;
+  if (!seen) {
+    if (g_seen.size() >= kMaxSeen) g_seen.erase(g_seen.begin());
+    g_seen.push_back(k);
+    return hipSuccess;
+  }
+  hipGraphExec_t exec = nullptr;
+  const hipError_t e = build_rollout_graph(k, &exec);
+  if (e != hipSuccess) return e;
+  g_graphs.push_back(RolloutGraph{k, exec});
+  *out = exec;
+  return hipSuccess;
 }
 
 template <bool kTraj>
@@ -195,6 +384,33 @@ hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
     else hipLaunchKernelGGL((k_fused_step<false, false>), g, b, 0, stream, p);
   }
   return hipGetLastError();
+}
+
+hipError_t launch_fused_graph(const StepParams &base, uint32_t T, void *workspace,
+                              hipStream_t stream, bool *used) {
+  *used = false;
+  if (base.n >= kObsStateMinEnvs || base.actions || T < kGraphMinSteps || T > kGraphMaxSteps)
+    return hipSuccess;
+  // A graph replays like launches on this stream only outside stream
+  // capture and on the current device.
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  hipError_t e = hipStreamIsCapturing(stream, &cap);
+  if (e != hipSuccess || cap != hipStreamCaptureStatusNone) return e;
+  int device = 0;
+  e = hipGetDevice(&device);
+  if (e != hipSuccess) return e;
+  if (stream != nullptr && hipGetStreamDeviceId(stream) != device) return hipSuccess;
+  RolloutKey key{device, base, T, workspace};
+  hipGraphExec_t exec = nullptr;
+  e = rollout_graph(key, &exec);
+  if (e != hipSuccess || !exec) return e;
+  hipLaunchKernelGGL(k_graph_set, dim3(1), dim3(64), 0, stream, GraphDesc{base.kact, base.t},
+                     static_cast<GraphDesc *>(workspace));
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  e = hipGraphLaunch(exec, stream);
+  *used = e == hipSuccess;
+  return e;
 }
 
 size_t concat_workspace_bytes(uint32_t n) { return size_t(n) * sizeof(f32x4); }

@@ -112,7 +112,7 @@ def test_output_alignment():
 def test_unfused_workspace_checks():
     need = cp.cp_workspace_bytes(1000, cp.CP_UNFUSED)
     assert need >= 1000 * 4 * 30
-    assert cp.cp_workspace_bytes(1000, cp.CP_FUSED) == 0
+    assert cp.cp_workspace_bytes(1000, cp.CP_RESIDENT) == 0
     assert cp.cp_workspace_bytes(0, cp.CP_UNFUSED) == 0
     assert call_step(handle(variant=cp.CP_UNFUSED)) == cp.CP_ERR_NULL
     h = handle(variant=cp.CP_UNFUSED, workspace=A, workspace_bytes=need - 1)
@@ -126,6 +126,17 @@ def test_concat_workspace_checks():
     assert call_step(handle(variant=cp.CP_CONCAT)) == cp.CP_ERR_NULL
     assert call_step(handle(variant=cp.CP_CONCAT, workspace=A + 4, workspace_bytes=need)) == cp.CP_ERR_ALIGN
     assert call_rollout(handle(variant=cp.CP_CONCAT, workspace=A, workspace_bytes=need - 16), 2) == cp.CP_ERR_SIZE
+
+
+def test_fused_workspace_is_optional_but_checked():
+    need = cp.cp_workspace_bytes(1000, cp.CP_FUSED)
+    # descriptor + an action word per wave of 64 and step, for 128 steps
+    assert need == 256 + 8 * 16 * 128
+    assert cp.cp_workspace_bytes(1 << 21, cp.CP_FUSED) == 0  # bandwidth-bound: none
+    assert call_rollout(handle(variant=cp.CP_FUSED), 0) == cp.CP_OK  # none: direct launches
+    assert call_rollout(handle(variant=cp.CP_FUSED, workspace=A + 8, workspace_bytes=need), 2) == cp.CP_ERR_ALIGN
+    assert call_rollout(handle(variant=cp.CP_FUSED, workspace=A, workspace_bytes=need - 1), 2) == cp.CP_ERR_SIZE
+    assert call_step(handle(variant=cp.CP_FUSED, workspace=A, workspace_bytes=need - 1)) == cp.CP_ERR_SIZE
 
 
 def test_policy_weights_alignment():

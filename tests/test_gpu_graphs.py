@@ -1,0 +1,113 @@
+"""Fused rollouts replayed from the library's HIP graphs (a call that
+repeats an earlier call's arrays, outputs and length) against the same
+rollouts launched step by step from the host: bit for bit, replay after
+replay, with the program's own work and synchronisations between calls,
+interleaved handles, and under a caller's own stream capture."""
+import pytest
+import torch
+
+import paper_2301_13062_amd as cp
+
+pytestmark = pytest.mark.gpu
+
+
+def twins(n, seed, env_base=0):
+    a = cp.CartPoleStates(n, variant=cp.CP_FUSED, env_base=env_base, graphs=True)
+    b = cp.CartPoleStates(n, variant=cp.CP_FUSED, env_base=env_base, graphs=False)
+    assert b.workspace is None
+    cp.cp_init(a, seed)
+    cp.cp_init(b, seed)
+    return a, b
+
+
+def assert_same(a, b, ta=None, tb=None):
+    assert torch.equal(a.state(), b.state())
+    assert torch.equal(a.ep_index, b.ep_index) and torch.equal(a.ep_len, b.ep_len)
+    assert a.t == b.t
+    if ta is not None:
+        for f in ("obs", "reward", "done", "done_count", "total_reward", "ret_sum", "totals"):
+            u, v = getattr(ta, f), getattr(tb, f)
+            assert (u is None) == (v is None), f
+            if u is not None:
+                assert torch.equal(u, v), f
+
+
+# 17: one word block; 300: three, the last one partial; env_base 37: waves
+# straddle two 64-environment action blocks
+@pytest.mark.parametrize("n,T,env_base", [(3001, 300, 0), (65536, 17, 0), (1000, 300, 37),
+                                          (63, 129, 5)])
+def test_repeated_rollouts_replay_bit_exact(gpu, n, T, env_base):
+    a, b = twins(n, seed=21, env_base=env_base)
+    assert a.workspace is not None
+    ta, tb = cp.Trajectory(n, T), cp.Trajectory(n, T)
+    junk = torch.randn(1 << 20, device="cuda")
+    for rep in range(4):  # the first call is recorded, later ones replay
+        cp.cp_rollout(a, T, 22, ta)
+        junk.mul_(0.5).add_(1.0)  # the program's own work between calls
+        cp.cp_rollout(b, T, 22, tb)
+        torch.cuda.synchronize()
+        assert_same(a, b, ta, tb)
+    # another action seed and a trajectory without stats, repeated
+    tc, td = cp.Trajectory(n, T, stats=False, reward=False), cp.Trajectory(n, T, stats=False, reward=False)
+    for rep in range(3):
+        cp.cp_rollout(a, T, 1000 + rep, tc)
+        cp.cp_rollout(b, T, 1000 + rep, td)
+        torch.cuda.synchronize()
+        assert_same(a, b, tc, td)
+    # no trajectory at all
+    for rep in range(3):
+        cp.cp_rollout(a, 50, 3, None)
+        cp.cp_rollout(b, 50, 3, None)
+    torch.cuda.synchronize()
+    assert_same(a, b)
+
+
+def test_interleaved_handles(gpu):
+    pairs = [twins(5000, seed=1), twins(777, seed=2, env_base=100)]
+    trajs = [(cp.Trajectory(5000, 64), cp.Trajectory(5000, 64)),
+             (cp.Trajectory(777, 64), cp.Trajectory(777, 64))]
+    for rep in range(4):
+        for (a, b), (ta, tb) in zip(pairs, trajs):
+            cp.cp_rollout(a, 64, 7, ta)
+            cp.cp_rollout(b, 64, 7, tb)
+        torch.cuda.synchronize()
+        for (a, b), (ta, tb) in zip(pairs, trajs):
+            assert_same(a, b, ta, tb)
+
+
+def test_large_batch_takes_no_workspace(gpu):
+    # from 2^21 environments a step is bandwidth-bound: no graph, no workspace
+    n = (1 << 21) + 5
+    a, b = twins(n, seed=3)
+    assert cp.cp_workspace_bytes(n, cp.CP_FUSED) == 0
+    ta, tb = cp.Trajectory(n, 20, stats=False), cp.Trajectory(n, 20, stats=False)
+    for rep in range(2):
+        cp.cp_rollout(a, 20, 4, ta)
+        cp.cp_rollout(b, 20, 4, tb)
+        torch.cuda.synchronize()
+        assert_same(a, b, ta, tb)
+
+
+def test_rollout_inside_caller_stream_capture(gpu):
+    # Under the caller's capture the library launches step by step (into the
+    # caller's graph); each replay repeats the captured step indices, so the
+    # reference rewinds its step counter before each call.
+    n, T = 4099, 40
+    a, b = twins(n, seed=5)
+    ta, tb = cp.Trajectory(n, T), cp.Trajectory(n, T)
+    cp.cp_rollout(a, T, 9, ta)  # a first call of this kind outside capture
+    cp.cp_rollout(b, T, 9, tb)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        cp.cp_rollout(a, T, 9, ta)
+    for rep in range(3):
+        g.replay()
+        torch.cuda.synchronize()
+        b.t = T
+        cp.cp_rollout(b, T, 9, tb)
+        torch.cuda.synchronize()
+        assert torch.equal(a.state(), b.state()), rep
+        assert torch.equal(a.ep_index, b.ep_index) and torch.equal(a.ep_len, b.ep_len), rep
+        for f in ("obs", "reward", "done", "totals"):
+            assert torch.equal(getattr(ta, f), getattr(tb, f)), (rep, f)
