@@ -203,3 +203,132 @@ def rollout(st: OracleState, T, act_seed=None, actions=None, policy_w=None, traj
                       _ptr(out["total_reward"], np.float32), _ptr(out["ret_sum"], np.uint32))
     st.t += T
     return out
+
+
+# --------------------------------------------------------------------------- other precisions
+F32, F64, F16 = 0, 1, 2
+PREC_DTYPE = {F32: np.float32, F64: np.float64, F16: np.float16}
+
+
+def _declare_prec(L):
+    if getattr(L, "_prec_declared", False):
+        return
+    L.orc_round_f16.argtypes = [ctypes.c_double]
+    L.orc_round_f16.restype = ctypes.c_double
+    for f in (L.orc_dynamics_f16,):
+        f.argtypes = [_p, ctypes.c_double, _p]
+        f.restype = None
+    for f in (L.orc_terminated_f64, L.orc_terminated_f16):
+        f.argtypes = [_p]
+        f.restype = ctypes.c_int
+    for f in (L.orc_reset_state_f64, L.orc_reset_state_f16):
+        f.argtypes = [_u64, _u32, _u32, _p]
+        f.restype = None
+    L.orc_init_prec.argtypes = [ctypes.c_int, _i64, _p, _u64, _p, _p, _p, _p, _p, _p]
+    L.orc_init_prec.restype = None
+    L.orc_rollout_prec.argtypes = [ctypes.c_int, _i64, _p, _p, _p, _p, _p, _p, _p, _u64, _u64,
+                                   _u64, _i64, _p, _p, _p, _p, _p, _p, _p]
+    L.orc_rollout_prec.restype = None
+    L._prec_declared = True
+
+
+def plib():
+    L = lib()
+    _declare_prec(L)
+    return L
+
+
+def round_f16(v):
+    return plib().orc_round_f16(float(v))
+
+
+def dynamics_f16(state, force):
+    """One binary16 step; state holds binary16 values (any float dtype)."""
+    s = np.ascontiguousarray(state, np.float64)
+    out = np.zeros(4, np.float64)
+    plib().orc_dynamics_f16(s.ctypes.data, float(force), out.ctypes.data)
+    return out
+
+
+def terminated_f64(state):
+    s = np.ascontiguousarray(state, np.float64)
+    return bool(plib().orc_terminated_f64(s.ctypes.data))
+
+
+def terminated_f16(state):
+    s = np.ascontiguousarray(state, np.float64)
+    return bool(plib().orc_terminated_f16(s.ctypes.data))
+
+
+def reset_state_f64(seed, env, episode):
+    out = np.zeros(4, np.float64)
+    plib().orc_reset_state_f64(seed, env, episode, out.ctypes.data)
+    return out
+
+
+def reset_state_f16(seed, env, episode):
+    out = np.zeros(4, np.float64)
+    plib().orc_reset_state_f16(seed, env, episode, out.ctypes.data)
+    return out
+
+
+class OracleStateP:
+    """SoA state of m environments at precision prec (F32, F64 or F16); the
+    state arrays have that precision's numpy dtype."""
+
+    def __init__(self, m, prec, env_ids=None):
+        self.m, self.prec = int(m), int(prec)
+        self.dtype = PREC_DTYPE[self.prec]
+        self.env_ids = None if env_ids is None else np.ascontiguousarray(env_ids, np.uint32)
+        for f in ("x", "x_dot", "theta", "theta_dot"):
+            setattr(self, f, np.zeros(m, self.dtype))
+        self.ep_index = np.zeros(m, np.uint32)
+        self.ep_len = np.zeros(m, np.uint32)
+        self.seed = 0
+        self.t = 0
+
+    def state(self):
+        return np.stack([self.x, self.x_dot, self.theta, self.theta_dot])
+
+
+def init_prec(st: OracleStateP, seed):
+    st.seed, st.t = int(seed), 0
+    s = [np.zeros(st.m, np.float64) for _ in range(4)]
+    plib().orc_init_prec(st.prec, st.m, _ptr(st.env_ids, np.uint32), st.seed,
+                         *(a.ctypes.data for a in s), st.ep_index.ctypes.data,
+                         st.ep_len.ctypes.data)
+    for f, a in zip(("x", "x_dot", "theta", "theta_dot"), s):
+        setattr(st, f, a.astype(st.dtype))
+
+
+def rollout_prec(st: OracleStateP, T, act_seed=None, actions=None, traj=False):
+    """Like rollout() at the state's precision (random or explicit actions);
+    obs comes back in the state's dtype."""
+    m, T = st.m, int(T)
+    act_seed = st.seed if act_seed is None else int(act_seed)
+    s = [np.ascontiguousarray(getattr(st, f), np.float64) for f in ("x", "x_dot", "theta", "theta_dot")]
+    out = {"done_count": np.zeros(m, np.uint32), "total_reward": np.zeros(m, np.float32),
+           "ret_sum": np.zeros(m, np.uint32)}
+    want = ("obs", "reward", "done") if traj is True else tuple(traj or ())
+    obs = np.zeros((T, 4, m), np.float64) if "obs" in want else None
+    if "reward" in want:
+        out["reward"] = np.zeros((T, m), np.float32)
+    if "done" in want:
+        out["done"] = np.zeros((T, m), np.uint8)
+    if actions is not None:
+        actions = np.ascontiguousarray(actions, np.uint8)
+        assert actions.shape == (T, m)
+    plib().orc_rollout_prec(st.prec, m, _ptr(st.env_ids, np.uint32), *(a.ctypes.data for a in s),
+                            st.ep_index.ctypes.data, st.ep_len.ctypes.data, st.seed, act_seed,
+                            st.t, T, _ptr(actions, np.uint8), _ptr(obs, np.float64),
+                            _ptr(out.get("reward"), np.float32), _ptr(out.get("done"), np.uint8),
+                            _ptr(out["done_count"], np.uint32),
+                            _ptr(out["total_reward"], np.float32), _ptr(out["ret_sum"], np.uint32))
+    for f, a in zip(("x", "x_dot", "theta", "theta_dot"), s):
+        converted = a.astype(st.dtype)
+        assert np.array_equal(converted.astype(np.float64), a)  # values of the precision
+        setattr(st, f, converted)
+    if obs is not None:
+        out["obs"] = obs.astype(st.dtype)
+    st.t += T
+    return out

@@ -326,3 +326,195 @@ void orc_rollout(int64_t m, const uint32_t *env_ids, float *x, float *x_dot, flo
         if (ret_sum) ret_sum[i] = returns;
     }
 }
+
+/* ------------------------------------------------------------------------ */
+/* Other precisions.  The hand-written CUDA port the paper compares against
+ * (Sec. "Comparison with CUDA implementation") ran the environment in
+ * binary16, binary32 and binary64; here the same step is also defined in
+ * binary64 and in binary16, every constant rounded once from its exact
+ * value and every operation rounded once to the working precision.          */
+
+/* Round to the nearest binary16 value, ties to even (IEEE 754 binary16: 11
+ * significant bits, exponents down to -14, subnormal quantum 2^-24, largest
+ * finite 65504).  The result is returned as a double holding that value.
+ * Scaling by a power of two is exact, and nearbyint rounds to nearest even
+ * in the default rounding mode.                                            */
+double orc_round_f16(double v)
+{
+    if (isnan(v) || isinf(v)) return v;
+    const double a = fabs(v);
+    if (a >= 65520.0) return copysign(INFINITY, v); /* 65504 + half an ulp and up */
+    int e;
+    frexp(a, &e);                    /* a = f * 2^e, 0.5 <= f < 1 (e = 0 for a = 0) */
+    int qexp = e - 11;               /* quantum of an 11-bit significand            */
+    if (qexp < -24) qexp = -24;      /* subnormal range                             */
+    const double q = ldexp(1.0, qexp);
+    return copysign(nearbyint(a / q) * q, v);
+}
+
+/* One binary16 operation: computed exactly (or correctly rounded) in
+ * binary64 and rounded once to binary16.  For +, -, * and / on binary16
+ * operands this equals the correctly rounded binary16 result: sums and
+ * products of binary16 values are exact in binary64, and a quotient rounded
+ * first to 53 and then to 11 bits rounds as if once (53 >= 2*11 + 2).        */
+static double h(double v) { return orc_round_f16(v); }
+
+/* The cart-pole step in binary16 (same equations, operation order and
+ * association as orc_dynamics_f32).  sin and cos are taken in binary64 and
+ * rounded once.  Values are passed as doubles holding binary16 values.      */
+void orc_dynamics_f16(const double s[4], double force, double out[4])
+{
+    const double g = h(9.8), mc = 1.0, mp = h(0.1), l = 0.5, tau = h(0.02);
+    const double m = h(mp + mc);
+    const double pml = h(mp * l);
+    const double four3 = h(4.0 / 3.0);
+    const double x = s[0], xd = s[1], th = s[2], thd = s[3];
+
+    const double c = h(cos(th));
+    const double sn = h(sin(th));
+    const double thd2 = h(thd * thd);
+    const double c2 = h(c * c);
+    const double temp = h(h(force + h(h(pml * thd2) * sn)) / m);
+    const double thacc = h(h(h(g * sn) - h(c * temp)) / h(l * h(four3 - h(h(mp * c2) / m))));
+    const double xacc = h(temp - h(h(h(pml * thacc) * c) / m));
+
+    out[0] = h(x + h(tau * xd));
+    out[1] = h(xd + h(tau * xacc));
+    out[2] = h(th + h(tau * thd));
+    out[3] = h(thd + h(tau * thacc));
+}
+
+/* Termination in binary64 and binary16: the limits 2.4 and 12 degrees
+ * rounded once to the working precision, strict comparisons.               */
+int orc_terminated_f64(const double s[4])
+{
+    const double x_limit = 2.4, th_limit = 12.0 * 2.0 * 3.14159265358979323846 / 360.0;
+    return s[0] < -x_limit || s[0] > x_limit || s[2] < -th_limit || s[2] > th_limit;
+}
+
+int orc_terminated_f16(const double s[4])
+{
+    const double x_limit = h(2.4), th_limit = h(12.0 * 2.0 * 3.14159265358979323846 / 360.0);
+    return s[0] < -x_limit || s[0] > x_limit || s[2] < -th_limit || s[2] > th_limit;
+}
+
+/* Start states.  binary64: the same 16-bit halves, centred and scaled by
+ * 0.1 * 2^-16 in binary64 (one rounding).  binary16: the binary32 start
+ * state rounded once to binary16.                                          */
+void orc_reset_state_f64(uint64_t seed, uint32_t env, uint32_t episode, double out[4])
+{
+    uint32_t key[2], u[2];
+    orc_stream_key(seed, ORC_TAG_RESET, key);
+    orc_threefry2x32(key[0], key[1], env, episode, u);
+    const uint32_t half[4] = {u[0] & 0xFFFFu, u[0] >> 16, u[1] & 0xFFFFu, u[1] >> 16};
+    const double scale = ldexp(0.1, -16);
+    for (int j = 0; j < 4; ++j)
+        out[j] = (double)((int32_t)half[j] - (int32_t)(1 << 15)) * scale;
+}
+
+void orc_reset_state_f16(uint64_t seed, uint32_t env, uint32_t episode, double out[4])
+{
+    float f[4];
+    orc_reset_state(seed, env, episode, f);
+    for (int j = 0; j < 4; ++j) out[j] = h((double)f[j]);
+}
+
+/* Initial draw and rollout at a given precision (ORC_F32, ORC_F64,
+ * ORC_F16), random or explicit actions, with the semantics of orc_init and
+ * orc_rollout.  State and obs arrays are doubles holding values of the
+ * working precision; reward, done and the statistics are as in orc_rollout. */
+enum { ORC_F32 = 0, ORC_F64 = 1, ORC_F16 = 2 };
+
+static void reset_prec(int prec, uint64_t seed, uint32_t env, uint32_t episode, double out[4])
+{
+    if (prec == ORC_F64) {
+        orc_reset_state_f64(seed, env, episode, out);
+    } else if (prec == ORC_F16) {
+        orc_reset_state_f16(seed, env, episode, out);
+    } else {
+        float f[4];
+        orc_reset_state(seed, env, episode, f);
+        for (int j = 0; j < 4; ++j) out[j] = f[j];
+    }
+}
+
+static int step_prec(int prec, double s[4], int action)
+{
+    double next[4];
+    int d;
+    if (prec == ORC_F64) {
+        orc_dynamics_f64(s, action ? 10.0 : -10.0, next);
+        d = orc_terminated_f64(next);
+    } else if (prec == ORC_F16) {
+        orc_dynamics_f16(s, action ? 10.0 : -10.0, next);
+        d = orc_terminated_f16(next);
+    } else {
+        float fs[4] = {(float)s[0], (float)s[1], (float)s[2], (float)s[3]}, fn[4];
+        orc_dynamics_f32(fs, orc_force(action), fn);
+        d = orc_terminated_f32(fn);
+        for (int j = 0; j < 4; ++j) next[j] = fn[j];
+    }
+    memcpy(s, next, sizeof next);
+    return d;
+}
+
+void orc_init_prec(int prec, int64_t m, const uint32_t *env_ids, uint64_t seed, double *x,
+                   double *x_dot, double *theta, double *theta_dot, uint32_t *ep_index,
+                   uint32_t *ep_len)
+{
+    for (int64_t i = 0; i < m; ++i) {
+        uint32_t env = env_ids ? env_ids[i] : (uint32_t)i;
+        double s[4];
+        reset_prec(prec, seed, env, 0u, s);
+        x[i] = s[0];
+        x_dot[i] = s[1];
+        theta[i] = s[2];
+        theta_dot[i] = s[3];
+        ep_index[i] = 0u;
+        ep_len[i] = 0u;
+    }
+}
+
+void orc_rollout_prec(int prec, int64_t m, const uint32_t *env_ids, double *x, double *x_dot,
+                      double *theta, double *theta_dot, uint32_t *ep_index, uint32_t *ep_len,
+                      uint64_t reset_seed, uint64_t act_seed, uint64_t t0, int64_t T,
+                      const uint8_t *actions, double *obs, float *reward, uint8_t *done,
+                      uint32_t *done_count, float *total_reward, uint32_t *ret_sum)
+{
+    for (int64_t i = 0; i < m; ++i) {
+        uint32_t env = env_ids ? env_ids[i] : (uint32_t)i;
+        double s[4] = {x[i], x_dot[i], theta[i], theta_dot[i]};
+        uint32_t k = ep_index[i], len = ep_len[i];
+        uint32_t n_done = 0u, returns = 0u;
+        float rsum = 0.0f;
+
+        for (int64_t step = 0; step < T; ++step) {
+            uint32_t t = (uint32_t)(t0 + (uint64_t)step);
+            int a = actions ? actions[step * m + i] != 0 : orc_action_bit(act_seed, env, t);
+            int d = step_prec(prec, s, a);
+            float r = 1.0f;
+            len += 1u;
+            rsum += r;
+            if (d) {
+                returns += len;
+                n_done += 1u;
+                len = 0u;
+                k += 1u;
+                reset_prec(prec, reset_seed, env, k, s);
+            }
+            if (obs)
+                for (int j = 0; j < 4; ++j) obs[(step * 4 + j) * m + i] = s[j];
+            if (reward) reward[step * m + i] = r;
+            if (done) done[step * m + i] = (uint8_t)d;
+        }
+        x[i] = s[0];
+        x_dot[i] = s[1];
+        theta[i] = s[2];
+        theta_dot[i] = s[3];
+        ep_index[i] = k;
+        ep_len[i] = len;
+        if (done_count) done_count[i] = n_done;
+        if (total_reward) total_reward[i] = rsum;
+        if (ret_sum) ret_sum[i] = returns;
+    }
+}
