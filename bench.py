@@ -92,6 +92,7 @@ def parse():
     ap.add_argument("--quick", action="store_true", help="headline only, no extra configs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", choices=["resident_1024x200", "resident_1048576x1000",
+                                       "resident_f64_1048576x1000", "resident_f16_1048576x1000",
                                        "streaming_16777216x100", "policy_4194304x500", "copy"],
                     help="run one workload only (for counter collection); prints its JSON")
     return ap.parse_args()
@@ -193,6 +194,10 @@ def bench_configs(cp, only=None):
         res["resident_1024x200"] = _resident_small(cp)
     if want("resident_1048576x1000"):
         res["resident_1048576x1000"] = _resident_large(cp)
+    if want("resident_f64_1048576x1000"):
+        res["resident_f64_1048576x1000"] = _resident_large(cp, "f64")
+    if want("resident_f16_1048576x1000"):
+        res["resident_f16_1048576x1000"] = _resident_large(cp, "f16")
     if want("streaming_16777216x100"):
         res["streaming_16777216x100"] = _streaming(cp)
     if want("policy_4194304x500"):
@@ -212,20 +217,23 @@ def _resident_small(cp):
     return {"env_steps_per_s": n * T * 20 / (ev * 1e-3), "ms": ev / 20}
 
 
-def _resident_large(cp):
-    # 1,048,576 x 1,000, register-resident, final state + per-env stats
+def _resident_large(cp, precision="f32"):
+    # 1,048,576 x 1,000, register-resident, final state + per-env stats; the
+    # op-rate peak of the precision (binary64 vector ops run at half the
+    # binary32 rate; binary16 ops, unpacked, at the binary32 rate)
     n, T = 1 << 20, 1000
-    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, precision=precision)
     cp.cp_init(s, 0)
     tr = cp.Trajectory(n, T, obs=False, reward=False, done=False)
     cp.cp_rollout(s, T, 0, tr)
     wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=5)
     mean_ms = ev / 5
     eps = n * T / (mean_ms * 1e-3)
+    peak = VALU_PEAK_TOPS / 2 if precision == "f64" else VALU_PEAK_TOPS
     return {"env_steps_per_s": eps, "ms": mean_ms,
             "roofline": {"bound": "alu", "achieved": eps * STEP_FLOPS / 1e12,
-                         "peak": VALU_PEAK_TOPS, "unit": "TOP/s",
-                         "frac": eps * STEP_FLOPS / 1e12 / VALU_PEAK_TOPS,
+                         "peak": peak, "unit": "TOP/s",
+                         "frac": eps * STEP_FLOPS / 1e12 / peak,
                          "ops_per_env_step": STEP_FLOPS}}
 
 

@@ -50,10 +50,27 @@ extern "C" {
 #define CP_OK 0
 #define CP_ERR_NULL (-1)        /* a required pointer is NULL                          */
 #define CP_ERR_SIZE (-2)        /* n, n_steps or workspace size out of range          */
-#define CP_ERR_ALIGN (-3)       /* a device pointer is not 4-byte aligned (u8: any)   */
+#define CP_ERR_ALIGN (-3)       /* a device pointer is misaligned for its element type */
 #define CP_ERR_RANGE (-4)       /* step counter or environment index would overflow   */
 #define CP_ERR_HIP (-5)         /* a HIP launch failed; see cp_last_error()           */
 #define CP_ERR_UNSUPPORTED (-6) /* combination not provided (e.g. policy + UNFUSED)    */
+
+/* Precision of the state, the step and the obs trajectory
+ * (cp_states.precision).  The paper's own implementation is binary32; the
+ * hand-written CUDA port it compares with ran binary16, binary32 and
+ * binary64 (Sec. "Comparison with CUDA implementation").  binary64 rounds
+ * every operation in binary64; binary16 rounds every operation to binary16
+ * (quotients: the binary32 quotient rounded once; sin, cos: the binary32
+ * values rounded once); start states are the binary32 draw's 16-bit halves
+ * scaled in binary64, or the binary32 start state rounded to binary16; the
+ * limits 2.4 and 12 degrees are rounded once to the precision.  CP_PREC_F64
+ * and CP_PREC_F16 are provided by cp_init and by CP_RESIDENT with random
+ * actions (no policy, no explicit actions); state arrays and obs then hold
+ * double / _Float16 values and must be aligned to their size.  reward,
+ * done and the statistics keep their types.                                */
+#define CP_PREC_F32 0
+#define CP_PREC_F64 1
+#define CP_PREC_F16 2
 
 #define CP_POLICY_WEIGHTS 4480 /* bf16 values: W1[4][64], W2[64][64], W3[64][2]       */
 #define CP_MAX_STEPS ((uint64_t)1 << 31) /* t + n_steps must stay below this       */
@@ -62,7 +79,8 @@ extern "C" {
  * env_base + i: that index keys its random actions and reset states, so a
  * batch split into several handles reproduces the undivided batch exactly. */
 typedef struct cp_states {
-    float *x, *x_dot, *theta, *theta_dot; /* [n] each, binary32                     */
+    float *x, *x_dot, *theta, *theta_dot; /* [n] each, binary32 (or the type of
+                                             `precision`, cast to float *)       */
     uint32_t *ep_index; /* [n] episodes completed since cp_init (keys the reset)   */
     uint32_t *ep_len;   /* [n] steps (= return) of the running episode             */
     int64_t n;          /* number of environments, 1 <= n <= 2^31 - 1              */
@@ -74,14 +92,19 @@ typedef struct cp_states {
     const uint16_t *policy_w; /* NULL = random actions; else CP_POLICY_WEIGHTS bf16
                                  bit patterns of the MLP policy (device memory,
                                  2-byte aligned), CP_RESIDENT only; see below      */
-    void *workspace;          /* CP_UNFUSED / CP_CONCAT temporaries, at least
-                                 cp_workspace_bytes(); CP_CONCAT: 16-B aligned */
+    void *workspace;          /* at least cp_workspace_bytes(n, variant) bytes:
+                                 CP_UNFUSED / CP_CONCAT temporaries (required;
+                                 CP_UNFUSED 4-B, CP_CONCAT 16-B aligned);
+                                 CP_FUSED: optional, 16-B aligned, enables graph
+                                 replay of repeated rollouts (see cp_rollout);
+                                 must not be shared by calls in flight together */
     size_t workspace_bytes;
     int64_t steps_per_launch; /* CP_RESIDENT rollouts: steps per kernel launch,
                                  the state going through HBM between launches
                                  (the paper's scan unroll factor); 0 = all the
                                  rollout's steps in one launch.  Results do not
                                  depend on it.                                  */
+    int32_t precision;        /* CP_PREC_F32 (0), CP_PREC_F64 or CP_PREC_F16     */
 } cp_states;
 
 /* MLP policy (the paper's "fuse simulation with neural network inference",
@@ -100,7 +123,8 @@ typedef struct cp_states {
  * environment, over this rollout: done_count, total_reward (the sum of the
  * rewards), ret_sum (sum of the returns of the episodes that ended in it).
  * global[0] += total terminations, global[1] += sum of those returns (the
- * caller clears global before the first call it wants counted).            */
+ * caller clears global before the first call it wants counted).  obs holds
+ * values of the handle's precision (double / _Float16 cast to float *).    */
 typedef struct cp_traj {
     float *obs;
     float *reward;
@@ -127,13 +151,20 @@ int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *reward, uin
  * stream of `seed` (or the MLP policy when s->policy_w is set), then
  * s->t += n_steps.  n_steps == 0 is a no-op.  Equivalent, bit for bit, to
  * n_steps calls of cp_step with the same action source.  traj may be NULL.
- * CP_UNFUSED and CP_FUSED launch one step at a time; CP_RESIDENT launches
- * ceil(n_steps / steps_per_launch) kernels (one when steps_per_launch is 0).
- * steps_per_launch < 0 is CP_ERR_SIZE.                                      */
+ * CP_UNFUSED, CP_CONCAT and CP_FUSED launch one step at a time; CP_RESIDENT
+ * launches ceil(n_steps / steps_per_launch) kernels (one when
+ * steps_per_launch is 0).  steps_per_launch < 0 is CP_ERR_SIZE.
+ * CP_FUSED with a workspace, below 2^21 environments, 16 to 8192 steps and
+ * outside stream capture: a call whose arrays, outputs, workspace and
+ * n_steps repeat those of an earlier call is replayed from one HIP graph
+ * that the library builds on that second call and keeps (at most 32 per
+ * process, for the life of the process); the first call of a kind launches
+ * step by step.  Results are the same either way.                          */
 int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
 
-/* Bytes of workspace CP_UNFUSED / CP_CONCAT need for n environments (0 for
- * the other variants, or for n out of range).                               */
+/* Bytes of workspace a variant takes for n environments: needed by
+ * CP_UNFUSED and CP_CONCAT, optional for CP_FUSED (graph replay; 0 from
+ * 2^21 environments on), 0 for CP_RESIDENT or for n out of range.          */
 size_t cp_workspace_bytes(int64_t n, int32_t variant);
 
 /* Message of the last failing call on this thread ("" if none).            */

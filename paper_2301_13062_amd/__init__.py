@@ -20,6 +20,9 @@ VARIANTS = {"unfused": CP_UNFUSED, "fused": CP_FUSED, "resident": CP_RESIDENT, "
 CP_OK, CP_ERR_NULL, CP_ERR_SIZE, CP_ERR_ALIGN, CP_ERR_RANGE, CP_ERR_HIP, CP_ERR_UNSUPPORTED = (
     0, -1, -2, -3, -4, -5, -6)
 CP_POLICY_WEIGHTS = 4480
+CP_PREC_F32, CP_PREC_F64, CP_PREC_F16 = 0, 1, 2
+PRECISIONS = {"f32": CP_PREC_F32, "f64": CP_PREC_F64, "f16": CP_PREC_F16}
+PREC_DTYPE = {CP_PREC_F32: torch.float32, CP_PREC_F64: torch.float64, CP_PREC_F16: torch.float16}
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "_build", "libcartpole.so")
@@ -33,7 +36,7 @@ class cp_states(ctypes.Structure):
                 ("env_base", ctypes.c_uint32), ("variant", ctypes.c_int32),
                 ("seed", ctypes.c_uint64), ("t", ctypes.c_uint64), ("stream", _p),
                 ("policy_w", _p), ("workspace", _p), ("workspace_bytes", ctypes.c_size_t),
-                ("steps_per_launch", ctypes.c_int64)]
+                ("steps_per_launch", ctypes.c_int64), ("precision", ctypes.c_int32)]
 
 
 class cp_traj(ctypes.Structure):
@@ -84,15 +87,18 @@ def _check(code):
 class CartPoleStates:
     """Device-resident batch state (structure of arrays) plus the handle.
 
-    x, x_dot, theta, theta_dot: float32 [n]; ep_index, ep_len: int32 [n]
+    x, x_dot, theta, theta_dot: [n] of the precision's dtype (float32 by
+    default; "f64" / "f16" for CP_RESIDENT); ep_index, ep_len: int32 [n]
     holding uint32 values.  ``seed`` and ``t`` mirror the handle's counters.
     """
 
     def __init__(self, n, variant=CP_FUSED, device="cuda", env_base=0, policy_w=None,
-                 workspace=None, steps_per_launch=0, graphs=True):
+                 workspace=None, steps_per_launch=0, graphs=True, precision=CP_PREC_F32):
         self.n, self.env_base = int(n), int(env_base)
         self.variant = VARIANTS.get(variant, variant)
-        f32 = dict(dtype=torch.float32, device=device)
+        self.precision = PRECISIONS.get(precision, precision)
+        self.dtype = PREC_DTYPE[self.precision]
+        f32 = dict(dtype=self.dtype, device=device)
         i32 = dict(dtype=torch.int32, device=device)
         self.x, self.x_dot = torch.empty(self.n, **f32), torch.empty(self.n, **f32)
         self.theta, self.theta_dot = torch.empty(self.n, **f32), torch.empty(self.n, **f32)
@@ -117,7 +123,7 @@ class CartPoleStates:
                       self.variant, self.seed, self.t, st.cuda_stream, _ptr(self.policy_w),
                       _ptr(self.workspace),
                       0 if self.workspace is None else self.workspace.numel(),
-                      self.steps_per_launch)
+                      self.steps_per_launch, self.precision)
         return h
 
     def _sync_back(self, h):
@@ -131,9 +137,10 @@ class Trajectory:
     """Optional rollout outputs (torch tensors, any may be None)."""
 
     def __init__(self, n, T, device="cuda", obs=True, reward=True, done=True, stats=True,
-                 totals=True):
+                 totals=True, dtype=torch.float32):
         f32 = dict(dtype=torch.float32, device=device)
-        self.obs = torch.empty((T, 4, n), **f32) if obs else None
+        # obs in the dtype of the handle's precision
+        self.obs = torch.empty((T, 4, n), dtype=dtype, device=device) if obs else None
         self.reward = torch.empty((T, n), **f32) if reward else None
         self.done = torch.empty((T, n), dtype=torch.uint8, device=device) if done else None
         self.done_count = torch.empty(n, dtype=torch.int32, device=device) if stats else None

@@ -29,6 +29,15 @@ int ok() {
 
 bool aligned4(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0u; }
 
+bool aligned_to(const void *p, uintptr_t bytes) {
+  return (reinterpret_cast<uintptr_t>(p) & (bytes - 1u)) == 0u;
+}
+
+// Bytes of one state / obs element at a precision.
+uintptr_t elem_bytes(int32_t precision) {
+  return precision == CP_PREC_F64 ? 8u : precision == CP_PREC_F16 ? 2u : 4u;
+}
+
 int check_states(const cp_states *s) {
   if (!s) return fail(CP_ERR_NULL, "cp_states pointer is NULL");
   if (!s->x || !s->x_dot || !s->theta || !s->theta_dot || !s->ep_index || !s->ep_len)
@@ -37,9 +46,15 @@ int check_states(const cp_states *s) {
     return fail(CP_ERR_SIZE, "n = %lld is outside [1, 2^31 - 1]", (long long)s->n);
   if (uint64_t(s->env_base) + uint64_t(s->n) > (uint64_t(1) << 32))
     return fail(CP_ERR_RANGE, "env_base + n exceeds 2^32");
-  if (!aligned4(s->x) || !aligned4(s->x_dot) || !aligned4(s->theta) || !aligned4(s->theta_dot) ||
-      !aligned4(s->ep_index) || !aligned4(s->ep_len))
-    return fail(CP_ERR_ALIGN, "state arrays must be 4-byte aligned");
+  if (s->precision != CP_PREC_F32 && s->precision != CP_PREC_F64 && s->precision != CP_PREC_F16)
+    return fail(CP_ERR_UNSUPPORTED, "unknown precision %d", (int)s->precision);
+  const uintptr_t eb = elem_bytes(s->precision);
+  if (!aligned_to(s->x, eb) || !aligned_to(s->x_dot, eb) || !aligned_to(s->theta, eb) ||
+      !aligned_to(s->theta_dot, eb))
+    return fail(CP_ERR_ALIGN, "state arrays must be aligned to their %u-byte elements",
+                unsigned(eb));
+  if (!aligned4(s->ep_index) || !aligned4(s->ep_len))
+    return fail(CP_ERR_ALIGN, "ep_index and ep_len must be 4-byte aligned");
   if (s->variant != CP_UNFUSED && s->variant != CP_FUSED && s->variant != CP_RESIDENT &&
       s->variant != CP_CONCAT)
     return fail(CP_ERR_UNSUPPORTED, "unknown variant %d", (int)s->variant);
@@ -111,12 +126,22 @@ cp::StepParams step_params(const cp_states *s, uint64_t act_seed) {
 
 }  // namespace
 
+// Stepping at binary64 / binary16: CP_RESIDENT with random actions only.
+int check_precision_step(const cp_states *s, bool explicit_actions) {
+  if (s->precision == CP_PREC_F32) return CP_OK;
+  if (s->variant != CP_RESIDENT || s->policy_w || explicit_actions)
+    return fail(CP_ERR_UNSUPPORTED,
+                "binary64 / binary16 states step in CP_RESIDENT with random actions only");
+  return CP_OK;
+}
+
 CP_API int cp_init(cp_states *s, uint64_t seed) {
   if (int e = check_states(s)) return e;
   const cp::U2 krst = cp::stream_key(seed, cp::kTagReset);
   hipStream_t st = static_cast<hipStream_t>(s->stream);
   if (int e = hip_status(cp::launch_init(s->x, s->x_dot, s->theta, s->theta_dot, s->ep_index,
-                                         s->ep_len, uint32_t(s->n), s->env_base, krst, st),
+                                         s->ep_len, uint32_t(s->n), s->env_base, krst,
+                                         s->precision, st),
                          "cp_init launch"))
     return e;
   s->seed = seed;
@@ -129,12 +154,13 @@ CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *rewa
   if (int e = check_states(s)) return e;
   if (int e = check_steps(s, 1)) return e;
   if (int e = check_workspace(s)) return e;
-  if ((obs && !aligned4(obs)) || (reward && !aligned4(reward)))
-    return fail(CP_ERR_ALIGN, "obs and reward must be 4-byte aligned");
+  if ((obs && !aligned_to(obs, elem_bytes(s->precision))) || (reward && !aligned4(reward)))
+    return fail(CP_ERR_ALIGN, "obs must be aligned to its elements, reward to 4 bytes");
   hipStream_t st = static_cast<hipStream_t>(s->stream);
   const bool policy = s->policy_w && !actions;
   if (policy && s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
+  if (int e = check_precision_step(s, actions != nullptr)) return e;
 
   hipError_t err;
   if (s->variant == CP_RESIDENT && !actions) {
@@ -148,6 +174,7 @@ CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *rewa
     p.t0 = sp.t; p.T = 1u;
     p.policy_w = policy ? s->policy_w : nullptr;
     p.obs = obs; p.reward = reward; p.done = done;
+    p.precision = s->precision;
     err = cp::launch_resident(p, st);
   } else {
     cp::StepParams p = step_params(s, s->seed);
@@ -170,13 +197,16 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
   if (int e = check_workspace(s)) return e;
   cp_traj none{};
   const cp_traj &tr = traj ? *traj : none;
-  if ((tr.obs && !aligned4(tr.obs)) || (tr.reward && !aligned4(tr.reward)) ||
+  if ((tr.obs && !aligned_to(tr.obs, elem_bytes(s->precision))) ||
+      (tr.reward && !aligned4(tr.reward)) ||
       (tr.done_count && !aligned4(tr.done_count)) ||
       (tr.total_reward && !aligned4(tr.total_reward)) || (tr.ret_sum && !aligned4(tr.ret_sum)) ||
       (tr.global && (reinterpret_cast<uintptr_t>(tr.global) & 7u)))
-    return fail(CP_ERR_ALIGN, "trajectory outputs must be 4-byte aligned (global: 8-byte)");
+    return fail(CP_ERR_ALIGN,
+                "trajectory outputs must be aligned to their elements (global: 8-byte)");
   if (s->policy_w && s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
+  if (int e = check_precision_step(s, false)) return e;
   if (s->steps_per_launch < 0)
     return fail(CP_ERR_SIZE, "steps_per_launch = %lld is negative", (long long)s->steps_per_launch);
   if (n_steps == 0) return ok();
@@ -192,13 +222,17 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
     p.policy_w = s->policy_w;
     p.done_count = tr.done_count; p.total_reward = tr.total_reward; p.ret_sum = tr.ret_sum;
     p.global = tr.global;
+    p.precision = s->precision;
     const int64_t chunk = s->steps_per_launch > 0 ? s->steps_per_launch : n_steps;
     for (int64_t j = 0; j < n_steps; j += chunk) {
       const int64_t len = chunk < n_steps - j ? chunk : n_steps - j;
       p.t0 = uint32_t(s->t + uint64_t(j));
       p.T = uint32_t(len);
       p.first = j == 0;
-      p.obs = tr.obs ? tr.obs + size_t(j) * 4u * n : nullptr;
+      // obs rows are 4 * n elements of the handle's precision
+      p.obs = tr.obs ? reinterpret_cast<float *>(reinterpret_cast<char *>(tr.obs) +
+                                                 size_t(j) * 4u * n * elem_bytes(s->precision))
+                     : nullptr;
       p.reward = tr.reward ? tr.reward + size_t(j) * n : nullptr;
       p.done = tr.done ? tr.done + size_t(j) * n : nullptr;
       if (int e = hip_status(cp::launch_resident(p, st), "cp_rollout launch")) {

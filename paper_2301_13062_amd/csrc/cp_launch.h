@@ -46,6 +46,8 @@ struct RolloutParams {
   uint32_t *ret_sum;         // [n]
   unsigned long long *global;
   uint32_t first;            // 1: per-env statistics start at this launch
+  int32_t precision;         // 0 binary32, 1 binary64, 2 binary16: the type of the
+                             // state and obs arrays (the resident kernel only)
 };
 
 // Batches from this size on with an obs trajectory read each step's state
@@ -70,8 +72,10 @@ inline size_t fused_workspace_bytes(uint32_t n) {
   return kGraphDescBytes + 8u * size_t(kWordRows) * ((size_t(n) + 63u) / 64u);
 }
 
-hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_index,
-                       uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst,
+// Episode-0 start states; x..thd point at values of the given precision
+// (0 binary32, 1 binary64, 2 binary16).
+hipError_t launch_init(void *x, void *xd, void *th, void *thd, uint32_t *ep_index,
+                       uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst, int precision,
                        hipStream_t stream);
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream);
 // A fused rollout of T steps with random actions from one cached HIP graph,

@@ -11,6 +11,7 @@
 #pragma once
 
 #include "cp_launch.h"
+#include "cp_precision.h"
 
 namespace cp {
 
@@ -82,7 +83,8 @@ struct HashPolicy {
     split = (first & 63u) != 0u;
   }
 
-  __device__ __forceinline__ uint32_t operator()(uint32_t j, uint32_t t, const State &) {
+  template <class St>
+  __device__ __forceinline__ uint32_t operator()(uint32_t j, uint32_t t, const St &) {
     if (j == 0u || (t & 63u) == 0u) {
       base = t & ~63u;
       const uint32_t step = base + (threadIdx.x & 63u);
@@ -103,35 +105,44 @@ struct HashPolicy {
 
 // The loop.  `policy(j, t, s)` returns the action of step t (j-th of this
 // rollout) for the lane's pre-step state s; it is called by every lane of
-// the wave at every step (policies may use cross-lane operations).
-template <bool kTraj, class Policy>
+// the wave at every step (policies may use cross-lane operations).  P is
+// the precision of the state, the step and the obs trajectory (the state
+// and obs pointers of p point at P::T values).
+template <bool kTraj, class Policy, class P = PrecF32>
 __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy &policy) {
+  using T = typename P::T;
+  using S = typename P::S;
+  T *const px = reinterpret_cast<T *>(p.x);
+  T *const pxd = reinterpret_cast<T *>(p.xd);
+  T *const pth = reinterpret_cast<T *>(p.th);
+  T *const pthd = reinterpret_cast<T *>(p.thd);
+  T *const pobs = reinterpret_cast<T *>(p.obs);
   const uint32_t i = blockIdx.x * kResidentBlock + threadIdx.x;
   const bool valid = i < p.n;
   const uint32_t env = p.env_base + i;
   // Lanes past the end run the loop on a dummy state (the wave stays
   // converged for the ballots), never terminate and store nothing.
-  State s{0.f, 0.f, 0.f, 0.f};
+  S s{T(0), T(0), T(0), T(0)};
   uint32_t k0 = 0u, len0 = 0u;
   if (valid) {
-    s = State{p.x[i], p.xd[i], p.th[i], p.thd[i]};
+    s = S{px[i], pxd[i], pth[i], pthd[i]};
     k0 = p.ep_index[i];
     len0 = p.ep_len[i];
   }
   uint32_t k = k0, len = len0;
   // Start state of the next episode, drawn ahead of time so that a
   // termination costs a select; `have` says whether it is drawn yet.
-  State nxt = reset_draw(p.krst, env, k + 1u);
+  S nxt = P::draw(p.krst, env, k + 1u);
   bool have = true;
   unsigned long long wave_done = 0u;
   for (uint32_t j = 0; j < p.T; ++j) {
     const uint32_t t = p.t0 + j;
     const uint32_t a = policy(j, t, s);
-    State o = dynamics(s, force_of(a));
-    const bool d = valid && terminated(o);
+    S o = P::step(s, a);
+    const bool d = valid && P::done(o);
     k += d ? 1u : 0u;
     len = d ? 0u : len + 1u;
-    if (d && !have) nxt = reset_draw(p.krst, env, k);  // second termination before a refill
+    if (d && !have) nxt = P::draw(p.krst, env, k);  // second termination before a refill
     if (d) o = nxt;
     have = have && !d;
     s = o;
@@ -139,10 +150,10 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
       const size_t base = size_t(j) * p.n + i;
       if (p.obs) {
         const size_t ob = size_t(j) * 4u * p.n + i;
-        __builtin_nontemporal_store(s.x, p.obs + ob);
-        __builtin_nontemporal_store(s.xd, p.obs + ob + p.n);
-        __builtin_nontemporal_store(s.th, p.obs + ob + 2u * p.n);
-        __builtin_nontemporal_store(s.thd, p.obs + ob + 3u * p.n);
+        __builtin_nontemporal_store(s.x, pobs + ob);
+        __builtin_nontemporal_store(s.xd, pobs + ob + p.n);
+        __builtin_nontemporal_store(s.th, pobs + ob + 2u * p.n);
+        __builtin_nontemporal_store(s.thd, pobs + ob + 3u * p.n);
       }
       if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + base);
       if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + base);
@@ -151,7 +162,7 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
     // batched refill: the lanes that used their prefetched state draw the
     // start state of the episode after the current one
     if ((j % kRefill) == kRefill - 1u && !have) {
-      nxt = reset_draw(p.krst, env, k + 1u);
+      nxt = P::draw(p.krst, env, k + 1u);
       have = true;
     }
   }
@@ -162,10 +173,10 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
   const uint32_t n_done = k - k0;
   const uint32_t returns = p.T + len0 - len;
   if (valid) {
-    p.x[i] = s.x;
-    p.xd[i] = s.xd;
-    p.th[i] = s.th;
-    p.thd[i] = s.thd;
+    px[i] = s.x;
+    pxd[i] = s.xd;
+    pth[i] = s.th;
+    pthd[i] = s.thd;
     p.ep_index[i] = k;
     p.ep_len[i] = len;
     // A rollout split over several launches adds to what the earlier

@@ -53,14 +53,17 @@ __device__ __forceinline__ T ld_global(const T *base, size_t i) {
 }
 
 
-__global__ __launch_bounds__(kBlock) void k_init(float *__restrict__ x, float *__restrict__ xd,
-                                                 float *__restrict__ th, float *__restrict__ thd,
+template <class P>
+__global__ __launch_bounds__(kBlock) void k_init(typename P::T *__restrict__ x,
+                                                 typename P::T *__restrict__ xd,
+                                                 typename P::T *__restrict__ th,
+                                                 typename P::T *__restrict__ thd,
                                                  uint32_t *__restrict__ ep_index,
                                                  uint32_t *__restrict__ ep_len, uint32_t n,
                                                  uint32_t env_base, U2 krst) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
   if (i >= n) return;
-  const State s = reset_draw(krst, env_base + i, 0u);
+  const typename P::S s = P::draw(krst, env_base + i, 0u);
   x[i] = s.x;
   xd[i] = s.xd;
   th[i] = s.th;
@@ -332,10 +335,10 @@ hipError_t rollout_graph(const RolloutKey &k, hipGraphExec_t *out) {
   return hipSuccess;
 }
 
-template <bool kTraj>
+template <bool kTraj, class P = PrecF32>
 __global__ __launch_bounds__(kResidentBlock) void k_resident(RolloutParams p) {
   HashPolicy policy(p.kact, p.env_base + blockIdx.x * kResidentBlock + threadIdx.x);
-  resident_rollout<kTraj>(p, policy);
+  resident_rollout<kTraj, HashPolicy, P>(p, policy);
 }
 
 // Totals of a per-step rollout from the episode counters: over T steps an
@@ -365,11 +368,24 @@ inline dim3 grid_for(uint32_t threads) { return dim3((threads + kBlock - 1) / kB
 
 }  // namespace
 
-hipError_t launch_init(float *x, float *xd, float *th, float *thd, uint32_t *ep_index,
-                       uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst,
-                       hipStream_t stream) {
-  hipLaunchKernelGGL(k_init, grid_for(n), dim3(kBlock), 0, stream, x, xd, th, thd, ep_index,
+template <class P>
+static void init_as(void *x, void *xd, void *th, void *thd, uint32_t *ep_index, uint32_t *ep_len,
+                    uint32_t n, uint32_t env_base, U2 krst, hipStream_t stream) {
+  using T = typename P::T;
+  hipLaunchKernelGGL(k_init<P>, grid_for(n), dim3(kBlock), 0, stream, static_cast<T *>(x),
+                     static_cast<T *>(xd), static_cast<T *>(th), static_cast<T *>(thd), ep_index,
                      ep_len, n, env_base, krst);
+}
+
+hipError_t launch_init(void *x, void *xd, void *th, void *thd, uint32_t *ep_index,
+                       uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst, int precision,
+                       hipStream_t stream) {
+  if (precision == 1)
+    init_as<PrecF64>(x, xd, th, thd, ep_index, ep_len, n, env_base, krst, stream);
+  else if (precision == 2)
+    init_as<PrecF16>(x, xd, th, thd, ep_index, ep_len, n, env_base, krst, stream);
+  else
+    init_as<PrecF32>(x, xd, th, thd, ep_index, ep_len, n, env_base, krst, stream);
   return hipGetLastError();
 }
 
@@ -426,14 +442,24 @@ hipError_t launch_concat_step(const StepParams &p, void *workspace, hipStream_t 
   return hipGetLastError();
 }
 
-hipError_t launch_resident(const RolloutParams &p, hipStream_t stream) {
-  if (p.policy_w) return launch_resident_policy(p, stream);
+template <class P>
+static void resident_as(const RolloutParams &p, hipStream_t stream) {
   const bool traj = p.obs || p.reward || p.done;
   const dim3 grid((p.n + kResidentBlock - 1) / kResidentBlock);
   if (traj)
-    hipLaunchKernelGGL(k_resident<true>, grid, dim3(kResidentBlock), 0, stream, p);
+    hipLaunchKernelGGL((k_resident<true, P>), grid, dim3(kResidentBlock), 0, stream, p);
   else
-    hipLaunchKernelGGL(k_resident<false>, grid, dim3(kResidentBlock), 0, stream, p);
+    hipLaunchKernelGGL((k_resident<false, P>), grid, dim3(kResidentBlock), 0, stream, p);
+}
+
+hipError_t launch_resident(const RolloutParams &p, hipStream_t stream) {
+  if (p.policy_w) return launch_resident_policy(p, stream);
+  if (p.precision == 1)
+    resident_as<PrecF64>(p, stream);
+  else if (p.precision == 2)
+    resident_as<PrecF16>(p, stream);
+  else
+    resident_as<PrecF32>(p, stream);
   return hipGetLastError();
 }
 

@@ -163,3 +163,35 @@ def test_product_path_does_not_touch_the_oracle():
                 assert "oracle" not in text.lower(), f
     out = subprocess.run(["nm", "-D", cp.LIB_PATH], capture_output=True, text=True).stdout
     assert "orc_" not in out
+
+
+@pytest.mark.parametrize("prec", [3, -1])
+def test_unknown_precision(prec):
+    h = handle(variant=cp.CP_RESIDENT, precision=prec)
+    assert call_init(h) == cp.CP_ERR_UNSUPPORTED
+    assert call_rollout(h, 2) == cp.CP_ERR_UNSUPPORTED
+
+
+def test_precision_alignment():
+    # binary64 state arrays need 8-byte alignment, binary16 obs 2-byte
+    h = handle(variant=cp.CP_RESIDENT, precision=cp.CP_PREC_F64, theta=A + 4)
+    assert call_init(h) == cp.CP_ERR_ALIGN and call_rollout(h, 2) == cp.CP_ERR_ALIGN
+    h = handle(variant=cp.CP_RESIDENT, precision=cp.CP_PREC_F16, x=A + 1)
+    assert call_init(h) == cp.CP_ERR_ALIGN
+    tr = cp.cp_traj(A + 4, None, None, None, None, None, None)
+    assert call_rollout(handle(variant=cp.CP_RESIDENT, precision=cp.CP_PREC_F64), 2, tr) == cp.CP_ERR_ALIGN
+    tr = cp.cp_traj(A + 1, None, None, None, None, None, None)
+    assert call_rollout(handle(variant=cp.CP_RESIDENT, precision=cp.CP_PREC_F16), 2, tr) == cp.CP_ERR_ALIGN
+
+
+@pytest.mark.parametrize("prec", [cp.CP_PREC_F64, cp.CP_PREC_F16])
+def test_precision_steps_in_resident_with_random_actions_only(prec):
+    for v in (cp.CP_FUSED, cp.CP_UNFUSED, cp.CP_CONCAT):
+        h = handle(variant=v, precision=prec, workspace=A,
+                   workspace_bytes=cp.cp_workspace_bytes(1000, cp.CP_UNFUSED))
+        assert call_step(h) == cp.CP_ERR_UNSUPPORTED and call_rollout(h, 2) == cp.CP_ERR_UNSUPPORTED
+    h = handle(variant=cp.CP_RESIDENT, precision=prec)
+    assert call_step(h, actions=A) == cp.CP_ERR_UNSUPPORTED  # explicit actions
+    h = handle(variant=cp.CP_RESIDENT, precision=prec, policy_w=A)
+    assert call_rollout(h, 2) == cp.CP_ERR_UNSUPPORTED and call_step(h) == cp.CP_ERR_UNSUPPORTED
+    assert h.t == 7
