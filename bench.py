@@ -93,7 +93,9 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", choices=["resident_1024x200", "resident_1048576x1000",
                                        "resident_f64_1048576x1000", "resident_f16_1048576x1000",
-                                       "streaming_16777216x100", "policy_4194304x500", "copy"],
+                                       "streaming_16777216x100", "policy_4194304x500",
+                                       "policy_separate_4194304x500",
+                                       "policy_two_streams_4194304x500", "copy"],
                     help="run one workload only (for counter collection); prints its JSON")
     return ap.parse_args()
 
@@ -202,6 +204,10 @@ def bench_configs(cp, only=None):
         res["streaming_16777216x100"] = _streaming(cp)
     if want("policy_4194304x500"):
         res["policy_4194304x500"] = _policy(cp)
+    if want("policy_separate_4194304x500"):
+        res["policy_separate_4194304x500"] = _policy_separate(cp, 1)
+    if want("policy_two_streams_4194304x500"):
+        res["policy_two_streams_4194304x500"] = _policy_separate(cp, 2)
     torch.cuda.empty_cache()
     return res
 
@@ -279,6 +285,52 @@ def _policy(cp):
             "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_MFMA_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": tflops / BF16_MFMA_PEAK_TFLOPS,
                          "flops_per_env_step": POLICY_FLOPS}}
+
+
+def _policy_separate(cp, streams):
+    """The same workload with simulation and inference as separate kernels
+    (the alternative to fusing them that the paper raises, Sec. "Future
+    Work"): per step cp_policy on the current state, then the fused step
+    with those explicit actions; with two streams the batch is split in two
+    halves whose launches are interleaved, so one half's inference can run
+    beside the other half's simulation."""
+    import numpy as np
+    import torch
+
+    from paper_2301_13062_amd import synth
+
+    n, T = 1 << 22, 500
+    w = torch.from_numpy(synth.policy_weights(0).view(np.int16)).cuda()
+    parts = []
+    for h in range(streams):
+        m, base = n // streams, h * (n // streams)
+        st = torch.cuda.Stream() if streams > 1 else torch.cuda.current_stream()
+        s = cp.CartPoleStates(m, variant=cp.CP_FUSED, env_base=base, graphs=False)
+        s.stream = st
+        obs = [torch.empty((4, m), device="cuda") for _ in range(2)]
+        parts.append({"s": s, "st": st, "obs": obs,
+                      "act": torch.empty(m, dtype=torch.uint8, device="cuda")})
+    torch.cuda.synchronize()
+    for p in parts:
+        with torch.cuda.stream(p["st"]):
+            cp.cp_init(p["s"], 0)
+            p["cur"] = torch.stack([p["s"].x, p["s"].x_dot, p["s"].theta, p["s"].theta_dot])
+
+    def steps(k):
+        for j in range(k):
+            for p in parts:
+                nxt = p["obs"][j % 2]
+                cp.cp_policy(p["cur"], w, p["act"], p["st"])
+                cp.cp_step(p["s"], p["act"], nxt, None, None)
+                p["cur"] = nxt
+
+    steps(10)
+    _sync()
+    t0 = time.perf_counter()
+    steps(T)
+    _sync()
+    ms = (time.perf_counter() - t0) * 1e3
+    return {"env_steps_per_s": n * T / (ms * 1e-3), "ms": ms, "streams": streams}
 
 
 CROSSOVER_N = (1, 4, 16, 64, 256, 1024, 4096)

@@ -162,6 +162,21 @@ int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *reward, uin
  * step by step.  Results are the same either way.                          */
 int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
 
+/* The MLP policy alone (above; weights as for cp_states.policy_w): for each
+ * of n environments, actions[i] = 1 (push right) or 0 for the state
+ * obs[0..3][i] (x, x_dot, theta, theta_dot planes of n binary32 values, as
+ * cp_step writes them).  With cp_step's explicit actions this runs
+ * simulation and inference as separate kernels -- on one stream, or
+ * pipelined over two streams -- the alternative to fusing them that the
+ * paper raises (Sec. "Future Work", item 1); the actions equal those of the
+ * fused CP_RESIDENT policy rollout.  obs, policy_w (2-byte aligned) and
+ * actions are device pointers; 1 <= n <= 2^31 - 1; asynchronous on
+ * `stream` (a hipStream_t; NULL = the null stream).  Returns CP_OK or
+ * CP_ERR_NULL / SIZE / ALIGN / HIP (nothing launched on a validation
+ * error).                                                                  */
+int cp_policy(const float *obs, int64_t n, const uint16_t *policy_w, uint8_t *actions,
+              void *stream);
+
 /* Bytes of workspace a variant takes for n environments: needed by
  * CP_UNFUSED and CP_CONCAT, optional for CP_FUSED (graph replay; 0 from
  * 2^21 environments on), 0 for CP_RESIDENT or for n out of range.          */

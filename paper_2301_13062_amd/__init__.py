@@ -65,6 +65,8 @@ def lib():
         L.cp_init.argtypes = [P(cp_states), ctypes.c_uint64]
         L.cp_step.argtypes = [P(cp_states), _p, _p, _p, _p]
         L.cp_rollout.argtypes = [P(cp_states), ctypes.c_int64, ctypes.c_uint64, P(cp_traj)]
+        L.cp_policy.argtypes = [_p, ctypes.c_int64, _p, _p, _p]
+        L.cp_policy.restype = ctypes.c_int
         L.cp_workspace_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32]
         L.cp_workspace_bytes.restype = ctypes.c_size_t
         L.cp_last_error.argtypes = []
@@ -171,6 +173,16 @@ def cp_rollout(states: CartPoleStates, n_steps: int, seed: int, traj: Trajectory
     _check(lib().cp_rollout(ctypes.byref(h), int(n_steps), int(seed),
                             ctypes.byref(th) if th is not None else None))
     states._sync_back(h)
+
+
+def cp_policy(obs, policy_w, actions, stream=None) -> None:
+    """actions[i] = the MLP policy's action for obs[:, i] (obs: float32 [4, n],
+    policy_w: bf16 bits [4480], actions: uint8 [n]); on torch's current
+    stream unless one is given."""
+    n = actions.numel()
+    assert obs.shape == (4, n) and obs.dtype == torch.float32 and obs.is_contiguous()
+    st = stream if stream is not None else torch.cuda.current_stream()
+    _check(lib().cp_policy(_ptr(obs), n, _ptr(policy_w), _ptr(actions), st.cuda_stream))
 
 
 def cp_workspace_bytes(n: int, variant: int) -> int:

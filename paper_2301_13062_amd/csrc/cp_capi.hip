@@ -310,6 +310,21 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
   return ok();
 }
 
+CP_API int cp_policy(const float *obs, int64_t n, const uint16_t *policy_w, uint8_t *actions,
+                     void *stream) {
+  if (!obs || !policy_w || !actions)
+    return fail(CP_ERR_NULL, "obs, policy_w and actions must not be NULL");
+  if (n < 1 || n > INT32_MAX)
+    return fail(CP_ERR_SIZE, "n = %lld is outside [1, 2^31 - 1]", (long long)n);
+  if (!aligned4(obs) || !aligned_to(policy_w, 2u))
+    return fail(CP_ERR_ALIGN, "obs must be 4-byte and policy_w 2-byte aligned");
+  if (int e = hip_status(cp::launch_policy_actions(obs, uint32_t(n), policy_w, actions,
+                                                   static_cast<hipStream_t>(stream)),
+                         "cp_policy launch"))
+    return e;
+  return ok();
+}
+
 CP_API size_t cp_workspace_bytes(int64_t n, int32_t variant) {
   if (n < 1 || n > INT32_MAX) return 0;
   return workspace_need(variant, uint32_t(n));

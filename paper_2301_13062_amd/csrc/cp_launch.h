@@ -90,6 +90,9 @@ hipError_t launch_fused_graph(const StepParams &base, uint32_t T, void *workspac
 // actions (launch_resident_policy), otherwise the random action stream.
 hipError_t launch_resident(const RolloutParams &p, hipStream_t stream);
 hipError_t launch_resident_policy(const RolloutParams &p, hipStream_t stream);
+// The MLP policy alone: actions[i] (0/1) for the state obs[0..3][i].
+hipError_t launch_policy_actions(const float *obs, uint32_t n, const uint16_t *policy_w,
+                                 uint8_t *actions, hipStream_t stream);
 // global[0] += terminations, global[1] += finished returns of a per-step
 // rollout of T steps, from the episode counters read before (after=false)
 // and after (after=true, extra = n*T) the steps.

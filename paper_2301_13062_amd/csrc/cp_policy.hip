@@ -141,7 +141,41 @@ __global__ __launch_bounds__(kResidentBlock) void k_resident_policy(RolloutParam
   resident_rollout<kTraj>(p, policy);
 }
 
+// The policy alone (simulation and inference as separate kernels, the
+// alternative to fusing them): actions[i] = the MLP's action for the state
+// obs[0..3][i].  Blocks stage the weights once and stride over the batch;
+// lanes past the batch evaluate the last environment (every lane of a wave
+// takes part in the cross-lane exchanges) and store nothing.
+constexpr uint32_t kPolicyMaxBlocks = 2048;
+
+__global__ __launch_bounds__(kResidentBlock) void k_policy_actions(
+    const float *__restrict__ obs, uint32_t n, const uint16_t *__restrict__ policy_w,
+    uint8_t *__restrict__ actions) {
+  __shared__ uint16_t w[kWeights];
+  for (int idx = threadIdx.x; idx < kWeights; idx += kResidentBlock) w[idx] = policy_w[idx];
+  __syncthreads();
+  MlpPolicy policy;
+  policy.load(w);
+  for (uint32_t base = blockIdx.x * kResidentBlock; base < n;
+       base += gridDim.x * kResidentBlock) {
+    const uint32_t i = base + threadIdx.x;
+    const uint32_t ic = i < n ? i : n - 1u;
+    const State s{obs[ic], obs[n + ic], obs[2u * n + ic], obs[3u * n + ic]};
+    const uint32_t a = policy(0u, 0u, s);
+    if (i < n) actions[i] = uint8_t(a);
+  }
+}
+
 }  // namespace
+
+hipError_t launch_policy_actions(const float *obs, uint32_t n, const uint16_t *policy_w,
+                                 uint8_t *actions, hipStream_t stream) {
+  const uint32_t blocks = (n + kResidentBlock - 1) / kResidentBlock;
+  const dim3 grid(blocks < kPolicyMaxBlocks ? blocks : kPolicyMaxBlocks);
+  hipLaunchKernelGGL(k_policy_actions, grid, dim3(kResidentBlock), 0, stream, obs, n, policy_w,
+                     actions);
+  return hipGetLastError();
+}
 
 hipError_t launch_resident_policy(const RolloutParams &p, hipStream_t stream) {
   const bool traj = p.obs || p.reward || p.done;

@@ -195,3 +195,14 @@ def test_precision_steps_in_resident_with_random_actions_only(prec):
     h = handle(variant=cp.CP_RESIDENT, precision=prec, policy_w=A)
     assert call_rollout(h, 2) == cp.CP_ERR_UNSUPPORTED and call_step(h) == cp.CP_ERR_UNSUPPORTED
     assert h.t == 7
+
+
+def test_policy_alone_validation():
+    L = cp.lib()
+    assert L.cp_policy(None, 10, A, A, None) == cp.CP_ERR_NULL
+    assert L.cp_policy(A, 10, None, A, None) == cp.CP_ERR_NULL
+    assert L.cp_policy(A, 10, A, None, None) == cp.CP_ERR_NULL
+    assert L.cp_policy(A, 0, A, A, None) == cp.CP_ERR_SIZE
+    assert L.cp_policy(A, 2 ** 31, A, A, None) == cp.CP_ERR_SIZE
+    assert L.cp_policy(A + 2, 10, A, A, None) == cp.CP_ERR_ALIGN
+    assert L.cp_policy(A, 10, A + 1, A, None) == cp.CP_ERR_ALIGN

@@ -111,3 +111,18 @@ def test_rollout_inside_caller_stream_capture(gpu):
         assert torch.equal(a.ep_index, b.ep_index) and torch.equal(a.ep_len, b.ep_len), rep
         for f in ("obs", "reward", "done", "totals"):
             assert torch.equal(getattr(ta, f), getattr(tb, f)), (rep, f)
+
+
+def test_more_kinds_than_the_graph_cache_holds(gpu):
+    # 40 kinds of rollout (one length each), each called three times: past
+    # the cache's 32 graphs the library launches step by step; results equal
+    # the direct launches throughout (seen-list eviction included)
+    n = 300
+    a, b = twins(n, seed=13)
+    for rep in range(3):
+        for T in range(16, 56):
+            ta, tb = cp.Trajectory(n, T, stats=False), cp.Trajectory(n, T, stats=False)
+            cp.cp_rollout(a, T, T, ta)
+            cp.cp_rollout(b, T, T, tb)
+            torch.cuda.synchronize()
+            assert_same(a, b, ta, tb)

@@ -190,3 +190,70 @@ def test_policy_step_equals_rollout(gpu):
         cp.cp_step(h)
     torch.cuda.synchronize()
     assert torch.equal(h.state(), s.state())
+
+
+# --------------------------------------------------------------------------- policy alone
+def test_policy_alone_matches_oracle(gpu):
+    # cp_policy on arbitrary states: every action equals the oracle's except
+    # where the oracle's logits nearly tie
+    w = weights(3)
+    n = 4099
+    st4 = np.ascontiguousarray(synth.states(n, seed=41, kind="typical"))
+    obs = torch.from_numpy(st4).cuda()
+    act = torch.empty(n, dtype=torch.uint8, device="cuda")
+    cp.cp_policy(obs, torch.from_numpy(w.view(np.int16)).cuda(), act)
+    torch.cuda.synchronize()
+    g = act.cpu().numpy()
+    ref, margin = np.zeros(n, np.uint8), np.zeros(n)
+    for i in range(n):
+        a, logits = O.mlp_action(w, st4[:, i])
+        ref[i], margin[i] = a, abs(float(logits[1]) - float(logits[0]))
+    bad = g != ref
+    assert bad.mean() < 1e-3 and np.all(margin[bad] < NEAR_TIE), margin[bad]
+    assert 0.2 < g.mean() < 0.8  # both actions occur
+
+
+def separate_kernels(w, n, T, seed=0, env_base=0, stream=None):
+    """Simulation and inference as separate kernels per step: cp_policy on
+    the current state, then the fused step with those explicit actions."""
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    s = cp.CartPoleStates(n, variant=cp.CP_FUSED, env_base=env_base)
+    s.stream = stream
+    obs = torch.empty((T, 4, n), device="cuda")
+    done = torch.empty((T, n), dtype=torch.uint8, device="cuda")
+    act = torch.empty(n, dtype=torch.uint8, device="cuda")
+    with torch.cuda.stream(stream if stream is not None else torch.cuda.current_stream()):
+        cp.cp_init(s, seed)
+        cur = torch.stack([s.x, s.x_dot, s.theta, s.theta_dot])
+        for j in range(T):
+            cp.cp_policy(cur, wd, act, stream)
+            cp.cp_step(s, act, obs[j], None, done[j])
+            cur = obs[j]
+    return s, obs, done
+
+
+def test_separate_kernels_equal_fused_policy_rollout(gpu):
+    # the standalone policy and the in-kernel policy evaluate the same MLP on
+    # the same binary32 states, so the two structures agree bit for bit
+    w = weights(0)
+    n, T = 3001, 60
+    fs, ft = run_policy(w, n, T, seed=2)
+    s, obs, done = separate_kernels(w, n, T, seed=2)
+    torch.cuda.synchronize()
+    assert torch.equal(obs, ft.obs) and torch.equal(done, ft.done)
+    assert torch.equal(s.state(), fs.state()) and torch.equal(s.ep_index, fs.ep_index)
+
+
+def test_two_streams_pipelined_halves_equal_one_stream(gpu):
+    # two halves of a batch (env_base keeps their random streams), each on
+    # its own stream: the same results as the undivided batch
+    w = weights(0)
+    n, T, cut = 4000, 40, 2000
+    ref, robs, rdone = separate_kernels(w, n, T, seed=4)
+    sa, sb = torch.cuda.Stream(), torch.cuda.Stream()
+    torch.cuda.synchronize()
+    a, aobs, adone = separate_kernels(w, cut, T, seed=4, stream=sa)
+    b, bobs, bdone = separate_kernels(w, n - cut, T, seed=4, env_base=cut, stream=sb)
+    torch.cuda.synchronize()
+    assert torch.equal(torch.cat([aobs, bobs], 2), robs) and torch.equal(torch.cat([adone, bdone], 1), rdone)
+    assert torch.equal(torch.cat([a.state(), b.state()], 1), ref.state())
