@@ -66,8 +66,8 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 COUNTER_SOURCES = ["paper_2301_13062_amd/csrc/cp_step.hip", "paper_2301_13062_amd/csrc/cp_device.h",
                    "paper_2301_13062_amd/csrc/cp_launch.h", "paper_2301_13062_amd/csrc/cp_resident.h",
                    "paper_2301_13062_amd/csrc/cp_capi.hip", "paper_2301_13062_amd/build.py"]
-COUNTERS = {"sources_sha256_16": "d8734523cd7d24cc",
-            "fused_step_65536": {"fetch_kib": 816.9, "write_kib": 2702.8},
+COUNTERS = {"sources_sha256_16": "24dc72f27a9c63ce",
+            "fused_step_65536": {"fetch_kib": 816.9, "write_kib": 2703.8},
             "read_factor": 1.99995, "write_factor": 1.0}
 
 
@@ -91,7 +91,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--quick", action="store_true", help="headline only, no extra configs")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--only", choices=["resident_1024x200", "resident_1048576x1000",
+    ap.add_argument("--only", choices=["headline", "resident_1024x200", "resident_1048576x1000",
                                        "resident_f64_1048576x1000", "resident_f16_1048576x1000",
                                        "streaming_16777216x100", "policy_4194304x500",
                                        "policy_separate_4194304x500",
@@ -121,7 +121,7 @@ def timed(fn, reps=1):
     return (time.perf_counter() - t0) * 1e3, e0.elapsed_time(e1)
 
 
-def bench_headline(cp, K, W):
+def bench_headline(cp, K, W, legs=("fused", "fused_direct", "concat", "unfused")):
     import torch
 
     n = 65536
@@ -130,6 +130,8 @@ def bench_headline(cp, K, W):
                                   ("fused_direct", cp.CP_FUSED, False),
                                   ("concat", cp.CP_CONCAT, False),
                                   ("unfused", cp.CP_UNFUSED, False)):
+        if name not in legs:
+            continue
         s = cp.CartPoleStates(n, variant=variant, graphs=graphs)
         cp.cp_init(s, 0)
         tr = cp.Trajectory(n, K, stats=False, totals=False)
@@ -380,6 +382,43 @@ def crossover(cp, T=1000):
             "gpu_faster_from_n": min(faster) if faster else None}
 
 
+def config_oracle_rates():
+    """The oracle on one host thread for every configuration, on a
+    deterministic subset of its environments (every k-th global index; the
+    counter-keyed random streams make a subset's environments identical to
+    their full-batch selves): env-steps/s of the subset, not an
+    extrapolation."""
+    import numpy as np
+
+    import oracle as O
+    from paper_2301_13062_amd import synth
+
+    def run(name, n, T, stride, prec=None, traj=(), policy=False):
+        ids = np.arange(0, n, stride, dtype=np.uint32)
+        if prec is None:
+            o = O.OracleState(len(ids), ids)
+            O.init(o, 0)
+            w = synth.policy_weights(0) if policy else None
+            t0 = time.perf_counter()
+            O.rollout(o, T, policy_w=w, traj=traj)
+        else:
+            o = O.OracleStateP(len(ids), prec, ids)
+            O.init_prec(o, 0)
+            t0 = time.perf_counter()
+            O.rollout_prec(o, T, traj=traj)
+        dt = time.perf_counter() - t0
+        return name, {"value": len(ids) * T / dt, "unit": "env-steps/s", "cores": 1,
+                      "sample": f"every {stride}th of {n} envs ({len(ids)}) x {T} steps, {dt:.1f} s"}
+
+    return dict([
+        run("resident_1048576x1000", 1 << 20, 1000, 256),
+        run("resident_f64_1048576x1000", 1 << 20, 1000, 256, prec=O.F64),
+        run("resident_f16_1048576x1000", 1 << 20, 1000, 256, prec=O.F16),
+        run("streaming_16777216x100", 1 << 24, 100, 256, traj=True),
+        run("policy_4194304x500", 1 << 22, 500, 16384, policy=True),
+    ])
+
+
 def cpu_baseline():
     import oracle as O
 
@@ -408,6 +447,11 @@ def main():
     cp.lib()  # fails loudly without the built library
     assert torch.cuda.is_available(), "no HIP device"
     K, W = args.steps, args.warmup
+    if args.only == "headline":
+        # the headline's fused leg alone (graph replay after the warm-up)
+        n, head = bench_headline(cp, K, W, legs=("fused",))
+        print(json.dumps({"only": "headline", **head["fused"]}))
+        return
     if args.only:
         res = bench_copy() if args.only == "copy" else bench_configs(cp, args.only)[args.only]
         print(json.dumps({"only": args.only, **res}))
@@ -455,6 +499,7 @@ def main():
         line["cpu_baseline"] = cpu_baseline()
         if not args.quick:
             line["cpu_baseline"]["crossover"] = crossover(cp)
+            line["cpu_baseline"]["configs"] = config_oracle_rates()
     print(json.dumps(line))
 
 
