@@ -130,9 +130,19 @@ __device__ __forceinline__ void fused_rest(const StepParams &p, uint32_t i, uint
   store_step(p, i, o, len, d, ret);
 }
 
-template <bool kExplicit, bool kEager>
+// kStream: the step reads its state from other arrays than it writes (the
+// previous obs plane of a trajectory rollout), which nothing reads again;
+// non-temporal loads keep those lines out of the caches (measured: 135 ->
+// 129 us per launch at 16,777,216 environments, while for a step that
+// rewrites the arrays it reads they cost 15%).
+template <bool kExplicit, bool kEager, bool kStream = false>
 __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
-  const State s{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
+  State s;
+  if (kStream)
+    s = State{__builtin_nontemporal_load(p.xi + i), __builtin_nontemporal_load(p.xdi + i),
+              __builtin_nontemporal_load(p.thi + i), __builtin_nontemporal_load(p.thdi + i)};
+  else
+    s = State{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
   if (kExplicit) a = uint32_t(p.actions[i] != 0);
   fused_rest<kEager>(p, i, a, s, p.ep_len[i], kEager ? p.ep_index[i] : 0u);
 }
@@ -172,12 +182,12 @@ __global__ __launch_bounds__(kBlock) void k_concat_finish(StepParams p, const f3
   store_step(p, i, o, len, d, ret);
 }
 
-template <bool kExplicit, bool kEager>
+template <bool kExplicit, bool kEager, bool kStream = false>
 __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
   // random actions: one block per wave, before any lane leaves
   const uint32_t a = kExplicit ? 0u : action_bit_wave(p.kact, p.env_base + i, p.t);
-  if (i < p.n) fused_one<kExplicit, kEager>(p, i, a);
+  if (i < p.n) fused_one<kExplicit, kEager, kStream>(p, i, a);
 }
 
 // Graph replay of fused rollouts.  Launched one by one, a latency-bound
@@ -395,9 +405,12 @@ hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
   if (p.actions) {
     if (eager) hipLaunchKernelGGL((k_fused_step<true, true>), g, b, 0, stream, p);
     else hipLaunchKernelGGL((k_fused_step<true, false>), g, b, 0, stream, p);
+  } else if (eager) {
+    hipLaunchKernelGGL((k_fused_step<false, true>), g, b, 0, stream, p);
+  } else if (p.xi != p.x) {  // state read from elsewhere than it is written
+    hipLaunchKernelGGL((k_fused_step<false, false, true>), g, b, 0, stream, p);
   } else {
-    if (eager) hipLaunchKernelGGL((k_fused_step<false, true>), g, b, 0, stream, p);
-    else hipLaunchKernelGGL((k_fused_step<false, false>), g, b, 0, stream, p);
+    hipLaunchKernelGGL((k_fused_step<false, false>), g, b, 0, stream, p);
   }
   return hipGetLastError();
 }
