@@ -107,11 +107,11 @@ typedef struct cp_states {
     int32_t precision;        /* CP_PREC_F32 (0), CP_PREC_F64 or CP_PREC_F16     */
 } cp_states;
 
-/* MLP policy (the paper's "fuse simulation with neural network inference",
- * Sec. "Future Work"): 4 -> 64 -> 64 -> 2, no biases, tanh on both hidden
- * layers, action = 1 (push right) iff logit[1] > logit[0].  Weights are
- * bfloat16, row-major [in][out], concatenated W1[4][64], W2[64][64],
- * W3[64][2].  The observation is the pre-step state rounded to bfloat16;
+/* MLP policy (the simulation fused with neural-network inference that the
+ * paper proposes as future work, Sec. "Future Work"): 4 -> 64 -> 64 -> 2,
+ * no biases, tanh on both hidden layers, action = 1 (push right) iff
+ * logit[1] > logit[0].  Weights are bfloat16, row-major [in][out],
+ * concatenated W1[4][64], W2[64][64], W3[64][2].  The observation is the pre-step state rounded to bfloat16;
  * products are accumulated in binary32 on the matrix cores; hidden
  * activations are rounded to bfloat16 before the next layer.  Where two
  * logits are within the accumulation and rounding noise of each other the

@@ -18,8 +18,8 @@
  *     drawn here from the counter-based Threefry-2x32-20 generator -- the
  *     generator whose unfusable kernel the paper removes -- instead of a
  *     precomputed pool;
- *   - the "fuse simulation with neural network inference" extension
- *     (Sec. "Future Work", item 1) as a 4-64-64-2 tanh MLP policy.
+ *   - simulation fused with neural-network inference, the paper's first
+ *     future-work item (Sec. "Future Work"), as a 4-64-64-2 tanh MLP policy.
  *
  * Arithmetic: IEEE binary32, round-to-nearest-even, every operation rounded
  * (build with -ffp-contract=off, no fast-math), glibc sinf/cosf.  Every

@@ -372,3 +372,30 @@ def test_totals_accumulate_across_calls(gpu):
     torch.cuda.synchronize()
     assert tr.totals[0] > first[0]
     assert tr.totals[0] - first[0] == int(u32(tr.done_count).sum())
+
+
+@pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
+def test_largest_environment_and_step_indices(gpu, variant):
+    # the last 777 environment indices below 2^32 (the last action block
+    # partly filled, waves straddling blocks) and the last 60 step indices
+    # below 2^31
+    n, T = 777, 60
+    env_base = 2 ** 32 - n
+    t0 = 2 ** 31 - 1 - T
+    s = cp.CartPoleStates(n, variant=variant, env_base=env_base)
+    cp.cp_init(s, 17)
+    s.t = t0
+    tr = cp.Trajectory(n, T)
+    cp.cp_rollout(s, T, 18, tr)
+    torch.cuda.synchronize()
+    assert s.t == 2 ** 31 - 1
+    o = O.OracleState(n, np.arange(env_base, 2 ** 32, dtype=np.uint64).astype(np.uint32))
+    O.init(o, 17)
+    o.t = t0
+    out = O.rollout(o, T, act_seed=18, traj=True)
+    g, gk, gl = gpu_state(s)
+    assert np.array_equal(tr.done.cpu().numpy(), out["done"])
+    assert np.abs(g.astype(np.float64) - o.state()).max() <= ROLL_ABS
+    assert np.array_equal(gk, o.ep_index) and np.array_equal(gl, o.ep_len)
+    with pytest.raises(cp.CartPoleError):  # one more step would reach 2^31
+        cp.cp_step(s)
