@@ -419,6 +419,17 @@ def config_oracle_rates():
     ])
 
 
+def _host():
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((line.split(":", 1)[1].strip() for line in f
+                          if line.startswith("model name")), "")
+    except OSError:
+        pass
+    return {"nproc": os.cpu_count(), "cpu_model": model}
+
+
 def cpu_baseline():
     import oracle as O
 
@@ -428,9 +439,15 @@ def cpu_baseline():
     t0 = time.perf_counter()
     O.rollout(o, T, traj=("done",))
     dt = time.perf_counter() - t0
+    workers = min(16, os.cpu_count() or 1)
     return {"value": n * T / dt, "unit": "env-steps/s", "cores": 1, "kind": "oracle",
             "sample": f"the whole headline workload ({n} envs x {T} steps, random actions, "
-                      f"done flags kept) on one host thread, {dt:.1f} s"}
+                      f"done flags kept) on one host thread, {dt:.1f} s",
+            "all_cores": {"value": _oracle_rate(n, T, workers), "unit": "env-steps/s",
+                          "cores": workers,
+                          "sample": "the same workload split over independent environment "
+                                    "ranges, one thread each"},
+            "host": _host()}
 
 
 def main():
