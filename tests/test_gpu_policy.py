@@ -257,3 +257,27 @@ def test_two_streams_pipelined_halves_equal_one_stream(gpu):
     torch.cuda.synchronize()
     assert torch.equal(torch.cat([aobs, bobs], 2), robs) and torch.equal(torch.cat([adone, bdone], 1), rdone)
     assert torch.equal(torch.cat([a.state(), b.state()], 1), ref.state())
+
+
+def test_policy_alone_strides_over_large_batches(gpu):
+    # more environments than the kernel's 2,048 blocks cover in one pass
+    # (blocks stride over the batch) and a ragged tail; sampled against the
+    # oracle, plus agreement with the fused kernel's first step everywhere
+    w = weights(5)
+    n = 2048 * 256 * 2 + 77
+    st4 = np.ascontiguousarray(synth.states(n, seed=43, kind="typical"))
+    obs = torch.from_numpy(st4).cuda()
+    act = torch.full((n,), 7, dtype=torch.uint8, device="cuda")
+    wd = torch.from_numpy(w.view(np.int16)).cuda()
+    cp.cp_policy(obs, wd, act)
+    torch.cuda.synchronize()
+    g = act.cpu().numpy()
+    assert set(np.unique(g)) <= {0, 1}  # every environment written
+    rng = np.random.default_rng(3)
+    ids = np.unique(np.concatenate([rng.choice(n, 2000, replace=False), np.arange(n - 80, n)]))
+    bad = []
+    for i in ids:
+        a, logits = O.mlp_action(w, st4[:, i])
+        if a != g[i]:
+            bad.append(abs(float(logits[1]) - float(logits[0])))
+    assert len(bad) <= 2 and all(m < NEAR_TIE for m in bad), bad
