@@ -135,7 +135,8 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
   S nxt = P::draw(p.krst, env, k + 1u);
   bool have = true;
   unsigned long long wave_done = 0u;
-  for (uint32_t j = 0; j < p.T; ++j) {
+  // One step (the j-th of this rollout).
+  auto step = [&](uint32_t j) {
     const uint32_t t = p.t0 + j;
     const uint32_t a = policy(j, t, s);
     S o = P::step(s, a);
@@ -159,13 +160,21 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
       if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + base);
     }
     wave_done += __popcll(__ballot(d));
-    // batched refill: the lanes that used their prefetched state draw the
-    // start state of the episode after the current one
-    if ((j % kRefill) == kRefill - 1u && !have) {
+  };
+  // Steps in rounds of kRefill (unrolled: the refill test and the loop
+  // control once per round), then the remaining steps.  After each round
+  // the lanes that used their prefetched state draw the start state of the
+  // episode after the current one.
+  uint32_t j = 0;
+  for (; j + kRefill <= p.T; j += kRefill) {
+#pragma unroll
+    for (uint32_t r = 0; r < kRefill; ++r) step(j + r);
+    if (!have) {
       nxt = P::draw(p.krst, env, k + 1u);
       have = true;
     }
   }
+  for (; j < p.T; ++j) step(j);
   // Over the rollout an environment's terminations are the growth of its
   // episode index and its finished returns are T + len(start) - len(end);
   // the summed reward of T steps (1 each, accumulated in binary32) is T up
