@@ -18,12 +18,18 @@ _lib = None
 
 
 def lib():
-    """Load the oracle library, compiling it first if it has not been built."""
+    """Load the oracle library, compiling it first if it has not been built.
+
+    ORACLE_LIB, when set, names another build of the same source to load
+    instead (the mutation test loads deliberately broken copies this way)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.LIB):
-            _build.build()
-        _lib = ctypes.CDLL(_build.LIB)
+        path = os.environ.get("ORACLE_LIB")
+        if not path:
+            path = _build.LIB
+            if not os.path.exists(path):
+                _build.build()
+        _lib = ctypes.CDLL(path)
         _declare(_lib)
     return _lib
 

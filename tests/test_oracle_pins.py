@@ -16,7 +16,8 @@ one test:
   (1 - tau^2 l^2) per explicit-Euler step;
 * mirror symmetry, the termination limits, the reward and episode
   bookkeeping invariants;
-* the Threefry-2x32-20 known-answer vectors;
+* the Threefry-2x32-20 known-answer vectors, and the written definition of
+  how its outputs become stream keys, actions and start states;
 * the random-policy mean episode length of cart-pole (about 22 steps).
 """
 import math
@@ -43,6 +44,61 @@ def test_threefry_known_answers():
     for k0, k1, c0, c1, o0, o1 in rows:
         got = O.threefry2x32((int(k0, 16), int(k1, 16)), (int(c0, 16), int(c1, 16)))
         assert got == (int(o0, 16), int(o1, 16))
+
+
+def _threefry_py(key, ctr):
+    """Threefry-2x32 with 20 rounds from its published description (Salmon
+    et al., SC'11): key schedule (k0, k1, k0 ^ k1 ^ 0x1BD11BDA), rotation
+    constants 13 15 26 6 17 29 16 24, a key injection after every fourth
+    round; Python integers, independent of the C oracle."""
+    m = 0xFFFFFFFF
+    ks = (key[0], key[1], 0x1BD11BDA ^ key[0] ^ key[1])
+    x0, x1 = (ctr[0] + ks[0]) & m, (ctr[1] + ks[1]) & m
+    for r in range(20):
+        rot = (13, 15, 26, 6, 17, 29, 16, 24)[r % 8]
+        x0 = (x0 + x1) & m
+        x1 = ((x1 << rot) | (x1 >> (32 - rot))) & m
+        x1 ^= x0
+        if r % 4 == 3:
+            i = r // 4 + 1
+            x0 = (x0 + ks[i % 3]) & m
+            x1 = (x1 + ks[(i + 1) % 3] + i) & m
+    return x0, x1
+
+
+def test_python_threefry_known_answers():
+    for ln in open(os.path.join(GOLDEN, "threefry2x32_kat.txt")):
+        if ln.strip() and not ln.startswith("#"):
+            k0, k1, c0, c1, o0, o1 = [f for f in ln.split() if f != "->"]
+            assert _threefry_py((int(k0, 16), int(k1, 16)), (int(c0, 16), int(c1, 16))) == \
+                (int(o0, 16), int(o1, 16))
+
+
+@pytest.mark.parametrize("seed", [0, 1, 0x0123456789ABCDEF, 2 ** 64 - 1])
+def test_stream_layout_matches_its_definition(seed):
+    """The way generator outputs become keys, actions and start states is a
+    convention of this implementation (the paper only says both are random);
+    its written definition is the pin: seed -> key (high word, low word);
+    stream key = output on counter (tag, 0), tag 1 actions, 2 start states;
+    env's action at step t = bit (env mod 64) of the output on counter
+    (env div 64, t), bits 0-31 from the first word, least significant first;
+    start state of episode k = the four 16-bit halves of the output on
+    counter (env, k), low half of the first word first, centred and scaled
+    by 0.1 * 2^-16."""
+    key = (seed >> 32, seed & 0xFFFFFFFF)
+    ka, kr = _threefry_py(key, (1, 0)), _threefry_py(key, (2, 0))
+    assert O.stream_key(seed, 1) == ka and O.stream_key(seed, 2) == kr
+    scale = float(np.ldexp(np.float32(0.1), -16))
+    for env in (0, 1, 31, 32, 33, 63, 64, 100, 4095, 2 ** 32 - 1):
+        for t in (0, 1, 999, 2 ** 32 - 1):
+            w = _threefry_py(ka, (env // 64, t))
+            j = env % 64
+            assert O.action_bit(seed, env, t) == (w[j // 32] >> (j % 32)) & 1, (env, t)
+        for k in (0, 1, 7, 2 ** 32 - 1):
+            u = _threefry_py(kr, (env, k))
+            halves = (u[0] & 0xFFFF, u[0] >> 16, u[1] & 0xFFFF, u[1] >> 16)
+            want = np.array([np.float32((h - 2 ** 15) * scale) for h in halves], np.float64)
+            assert np.array_equal(np.asarray(O.reset_state(seed, env, k), np.float64), want), (env, k)
 
 
 def test_action_stream_balanced_and_uncorrelated():
