@@ -69,18 +69,19 @@ __device__ __forceinline__ void block_publish(unsigned long long *global, unsign
 // one generator output (see action_bit); every 64 steps each lane computes
 // the block of one of the next 64 steps (lane L: step base + L), and each
 // step reads its block from the owning lane (v_readlane) into scalar
-// registers.  A wave whose environments straddle two blocks computes both.
+// registers.  Waves start at multiples of 64 environments after the
+// launch's first one, so either every wave is aligned to a block
+// (kAligned: the launch starts at a multiple of 64) or every wave straddles
+// two blocks and computes both.
+template <bool kAligned>
 struct HashPolicy {
   U2 key;
   uint32_t env, g0;
-  bool split;
   U2 b0, b1;  // this lane's blocks for step base + lane
   uint32_t base;
 
   __device__ __forceinline__ HashPolicy(U2 k, uint32_t e) : key(k), env(e) {
-    const uint32_t first = __builtin_amdgcn_readfirstlane(e);
-    g0 = first >> 6;
-    split = (first & 63u) != 0u;
+    g0 = uint32_t(__builtin_amdgcn_readfirstlane(int(e))) >> 6;  // logical shift: e may be >= 2^31
   }
 
   template <class St>
@@ -89,16 +90,22 @@ struct HashPolicy {
       base = t & ~63u;
       const uint32_t step = base + (threadIdx.x & 63u);
       b0 = threefry2x32(key.a, key.b, g0, step);
-      if (split) b1 = threefry2x32(key.a, key.b, g0 + 1u, step);
+      if (!kAligned) b1 = threefry2x32(key.a, key.b, g0 + 1u, step);
     }
     const int src = int(t - base);
     U2 w{uint32_t(__builtin_amdgcn_readlane(int(b0.a), src)),
          uint32_t(__builtin_amdgcn_readlane(int(b0.b), src))};
-    if (split) {
-      const U2 w1{uint32_t(__builtin_amdgcn_readlane(int(b1.a), src)),
-                  uint32_t(__builtin_amdgcn_readlane(int(b1.b), src))};
-      if ((env >> 6) != g0) w = w1;
+    if (kAligned) {
+      // Lane L is environment 64*g0 + L, so the block word is the wave's
+      // lane mask of pushes to the right: the action is one select on it.
+      return __builtin_amdgcn_inverse_ballot_w64(
+                 (static_cast<unsigned long long>(w.b) << 32) | w.a)
+                 ? 1u
+                 : 0u;
     }
+    const U2 w1{uint32_t(__builtin_amdgcn_readlane(int(b1.a), src)),
+                uint32_t(__builtin_amdgcn_readlane(int(b1.b), src))};
+    if ((env >> 6) != g0) w = w1;
     return bit_of_block(w, env);
   }
 };

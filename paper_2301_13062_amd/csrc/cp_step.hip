@@ -345,10 +345,10 @@ hipError_t rollout_graph(const RolloutKey &k, hipGraphExec_t *out) {
   return hipSuccess;
 }
 
-template <bool kTraj, class P = PrecF32>
+template <bool kTraj, class P, bool kAligned>
 __global__ __launch_bounds__(kResidentBlock) void k_resident(RolloutParams p) {
-  HashPolicy policy(p.kact, p.env_base + blockIdx.x * kResidentBlock + threadIdx.x);
-  resident_rollout<kTraj, HashPolicy, P>(p, policy);
+  HashPolicy<kAligned> policy(p.kact, p.env_base + blockIdx.x * kResidentBlock + threadIdx.x);
+  resident_rollout<kTraj, HashPolicy<kAligned>, P>(p, policy);
 }
 
 // Totals of a per-step rollout from the episode counters: over T steps an
@@ -455,14 +455,22 @@ hipError_t launch_concat_step(const StepParams &p, void *workspace, hipStream_t 
   return hipGetLastError();
 }
 
-template <class P>
+template <class P, bool kAligned>
 static void resident_as(const RolloutParams &p, hipStream_t stream) {
   const bool traj = p.obs || p.reward || p.done;
   const dim3 grid((p.n + kResidentBlock - 1) / kResidentBlock);
   if (traj)
-    hipLaunchKernelGGL((k_resident<true, P>), grid, dim3(kResidentBlock), 0, stream, p);
+    hipLaunchKernelGGL((k_resident<true, P, kAligned>), grid, dim3(kResidentBlock), 0, stream, p);
   else
-    hipLaunchKernelGGL((k_resident<false, P>), grid, dim3(kResidentBlock), 0, stream, p);
+    hipLaunchKernelGGL((k_resident<false, P, kAligned>), grid, dim3(kResidentBlock), 0, stream, p);
+}
+
+template <class P>
+static void resident_as(const RolloutParams &p, hipStream_t stream) {
+  if (p.env_base % 64u == 0u)
+    resident_as<P, true>(p, stream);
+  else
+    resident_as<P, false>(p, stream);
 }
 
 hipError_t launch_resident(const RolloutParams &p, hipStream_t stream) {

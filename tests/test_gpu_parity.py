@@ -374,13 +374,15 @@ def test_totals_accumulate_across_calls(gpu):
     assert tr.totals[0] - first[0] == int(u32(tr.done_count).sum())
 
 
+@pytest.mark.parametrize("top", [0, 55], ids=["straddling", "aligned"])
 @pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
-def test_largest_environment_and_step_indices(gpu, variant):
-    # the last 777 environment indices below 2^32 (the last action block
-    # partly filled, waves straddling blocks) and the last 60 step indices
-    # below 2^31
+def test_largest_environment_and_step_indices(gpu, variant, top):
+    # 777 environments ending `top` below 2^32 (top 0: the last action block
+    # partly filled and every wave straddling two blocks; top 55: waves
+    # aligned to blocks, the last one partly filled), all indices >= 2^31,
+    # and the last 60 step indices below 2^31
     n, T = 777, 60
-    env_base = 2 ** 32 - n
+    env_base = 2 ** 32 - n - top
     t0 = 2 ** 31 - 1 - T
     s = cp.CartPoleStates(n, variant=variant, env_base=env_base)
     cp.cp_init(s, 17)
@@ -389,7 +391,7 @@ def test_largest_environment_and_step_indices(gpu, variant):
     cp.cp_rollout(s, T, 18, tr)
     torch.cuda.synchronize()
     assert s.t == 2 ** 31 - 1
-    o = O.OracleState(n, np.arange(env_base, 2 ** 32, dtype=np.uint64).astype(np.uint32))
+    o = O.OracleState(n, np.arange(env_base, env_base + n, dtype=np.uint64).astype(np.uint32))
     O.init(o, 17)
     o.t = t0
     out = O.rollout(o, T, act_seed=18, traj=True)
