@@ -67,8 +67,8 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 # stand for it only while these are unchanged.
 COUNTER_SOURCES = ["paper_2301_13062_amd/csrc/cp_step.hip", "paper_2301_13062_amd/csrc/cp_device.h",
                    "paper_2301_13062_amd/csrc/cp_launch.h", "paper_2301_13062_amd/build.py"]
-COUNTERS = {"sources_sha256_16": "8cb557b19b4a65d1",
-            "fused_step_65536": {"fetch_kib": 813.4, "write_kib": 2703.4},
+COUNTERS = {"sources_sha256_16": "96b74da729a3867e",
+            "fused_step_65536": {"fetch_kib": 812.5, "write_kib": 2703.9},
             "read_factor": 1.99995, "write_factor": 1.0}
 
 
@@ -96,7 +96,8 @@ def parse():
                                        "resident_f64_1048576x1000", "resident_f16_1048576x1000",
                                        "streaming_16777216x100", "policy_4194304x500",
                                        "policy_separate_4194304x500",
-                                       "policy_two_streams_4194304x500", "copy"],
+                                       "policy_two_streams_4194304x500", "copy",
+                                       "valu_reference"],
                     help="run one workload only (for counter collection); prints its JSON")
     return ap.parse_args()
 
@@ -188,6 +189,46 @@ def bench_copy():
     wall, ev = timed(lambda: torch.mul(src, 1.0, out=dst), reps=5)
     return {"bytes_read": 1 << 30, "bytes_written": 1 << 30, "ms": ev / 5,
             "GB_per_s": 2 * (1 << 30) / (ev / 5 * 1e-3) / 1e9}
+
+
+VALU_REFERENCE_FORMS = ("fma_f32_vgpr", "fma_f32_sgpr_operand", "rotate_u32", "rcp_f32")
+
+
+def bench_valu_reference():
+    """Vector-instruction issue rates this GPU sustains, per instruction
+    class: eight independent chains of one form per lane, eight waves per
+    SIMD, no memory traffic (reference kernels in their own library).  Forms:
+    binary32 FMA on vector registers; the same with a wave-uniform scalar
+    operand; a 32-bit rotation (the generator's); the binary32 reciprocal.
+    They are the practical ceilings for the VALU-bound kernels' instruction
+    mixes; the FMA form is also given as a fraction of the op-rate peak."""
+    import ctypes
+
+    import torch
+
+    from paper_2301_13062_amd import build as B
+
+    ref = ctypes.CDLL(B.REF_LIB)
+    ref.cpref_chains.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                 ctypes.c_void_p]
+    blocks, iters = 256 * 8, 2000  # blocks of 4 waves: 8 waves per SIMD on 256 CUs
+    out = torch.empty(blocks * 256, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    res = {}
+    for form, name in enumerate(VALU_REFERENCE_FORMS):
+        def call():
+            if ref.cpref_chains(form, blocks, iters, out.data_ptr(), stream) != 0:
+                raise RuntimeError("reference kernel failed to launch")
+
+        call()
+        wall, ev = timed(call, reps=5)
+        ms = ev / 5
+        rate = blocks * 4 * iters * ref.cpref_ops_per_iter() / (ms * 1e-3)  # wave64 instr/s
+        res[name] = {"ms": ms, "wave64_per_cu_per_ns": rate / 256 / 1e9}
+    fma = res["fma_f32_vgpr"]["wave64_per_cu_per_ns"] * 256e9 * 64
+    res["fma_f32_vgpr"].update({"lane_ops_per_s": fma,
+                                "frac_of_op_peak": fma / (VALU_PEAK_TOPS * 1e12)})
+    return res
 
 
 def bench_configs(cp, only=None):
@@ -471,7 +512,8 @@ def main():
         print(json.dumps({"only": "headline", **head["fused"]}))
         return
     if args.only:
-        res = bench_copy() if args.only == "copy" else bench_configs(cp, args.only)[args.only]
+        refs = {"copy": bench_copy, "valu_reference": bench_valu_reference}
+        res = refs[args.only]() if args.only in refs else bench_configs(cp, args.only)[args.only]
         print(json.dumps({"only": args.only, **res}))
         return
 
@@ -513,6 +555,7 @@ def main():
     if not args.quick:
         line["configs"] = bench_configs(cp)
         line["unroll"] = bench_unroll(cp)
+        line["references"] = {"copy": bench_copy(), "valu": bench_valu_reference()}
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline()
         if not args.quick:

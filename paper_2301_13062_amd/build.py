@@ -10,6 +10,10 @@ OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(OUT_DIR, "libcartpole.so")
 
 SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip"]
+# A measurement reference (the sustained vector-FMA issue rate), in a library
+# of its own that only the benchmark loads.
+REF_SOURCES = ["ref_valu.hip"]
+REF_LIB = os.path.join(OUT_DIR, "libcpref.so")
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -26,17 +30,22 @@ FLAGS = [
 ]
 
 
-def build(verbose=False) -> str:
-    os.makedirs(OUT_DIR, exist_ok=True)
-    tmp = LIB + ".tmp"
+def _hipcc(sources, out, verbose):
+    tmp = out + ".tmp"
     cmd = ["hipcc", *FLAGS, f"-I{INCLUDE}", f"-I{CSRC}",
-           *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
+           *[os.path.join(CSRC, s) for s in sources], "-o", tmp]
     if verbose:
         print(" ".join(cmd))
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"hipcc failed:\n{r.stderr}")
-    os.replace(tmp, LIB)
+    os.replace(tmp, out)
+
+
+def build(verbose=False) -> str:
+    os.makedirs(OUT_DIR, exist_ok=True)
+    _hipcc(SOURCES, LIB, verbose)
+    _hipcc(REF_SOURCES, REF_LIB, verbose)
     return LIB
 
 

@@ -36,6 +36,18 @@ def test_library_exports_every_declared_symbol():
     assert exported == names  # nothing undeclared leaks out
 
 
+def test_reference_library_is_separate():
+    # the issue-rate reference kernels live in their own library, which only
+    # the benchmark loads; the cart-pole library exports none of it
+    from paper_2301_13062_amd import build as B
+
+    out = subprocess.run(["nm", "-D", "--defined-only", B.REF_LIB], capture_output=True,
+                         text=True, check=True).stdout
+    assert sorted(set(re.findall(r"\bT (\w+)", out))) == ["cpref_chains", "cpref_ops_per_iter"]
+    main = subprocess.run(["nm", "-D", cp.LIB_PATH], capture_output=True, text=True).stdout
+    assert "cpref_" not in main
+
+
 def handle(**kw):
     h = cp.cp_states(A, A + 0x1000, A + 0x2000, A + 0x3000, A + 0x4000, A + 0x5000, 1000, 0,
                      cp.CP_FUSED, 123, 7, None, None, None, 0)
