@@ -4,7 +4,9 @@
 // future-work item, Sec. "Future Work").
 //
 // Per step each wave evaluates the policy for its 64 environments as four
-// 16-environment tiles.  Every dense layer is a chain of
+// 16-environment tiles, two at a time (two independent chains of matrix
+// products and tanh for the scheduler to interleave).  Every dense layer is
+// a chain of
 // v_mfma_f32_16x16x16_bf16 with the weights as the A operand (neurons =
 // rows) and the environments as the B operand (columns): lane 16g+c holds
 // A[c][4g..4g+3], B[4g..4g+3][c] and D[4g..4g+3][c].  Since a layer's D
@@ -14,7 +16,10 @@
 // leaving the lane.  Only the layer-1 inputs (the observation, gathered from
 // the lane that owns the environment) and the chosen actions (scattered
 // back) cross lanes, through ds_bpermute.  The 8,960 bytes of bf16 weights
-// are staged once per block through LDS into register fragments.
+// are staged once per block in LDS; the layer-1 and layer-3 fragments are
+// then held in registers, the 16 layer-2 fragments are read from LDS at
+// every use (held in registers they would leave room for one tile at a
+// time only).
 #include "cp_launch.h"
 #include "cp_resident.h"
 
@@ -78,20 +83,34 @@ __device__ __forceinline__ f32x4 mma(bf16x4 a, bf16x4 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(a, b, c, 0, 0, 0);
 }
 
+// Layer-2 weight fragments in LDS in the order the lanes read them:
+// fragment (m, kc) of lane L (rows 16m.., K chunk 16kc.. of W2^T) at
+// [(4m + kc) * 64 + L], 8 bytes, so that a wave reads one fragment with one
+// conflict-free ds_read_b64.  `w` is the staged row-major [in][out] array.
+constexpr int kW2Frags = 16 * 64;
+
+__device__ __forceinline__ void stage_w2_fragments(const uint16_t *w, bf16x4 *w2f) {
+  for (int idx = threadIdx.x; idx < kW2Frags; idx += kResidentBlock) {
+    const int mk = idx >> 6, lane = idx & 63, m = mk >> 2, kc = mk & 3;
+    const int g = lane >> 4, c = lane & 15;
+    bf16x4 f;
+    for (int j = 0; j < 4; ++j) f[j] = short(w[kOffW2 + (16 * kc + 4 * g + j) * kHid + 16 * m + c]);
+    w2f[idx] = f;
+  }
+}
+
 struct MlpPolicy {
-  bf16x4 w1[4];     // W1^T rows 16m..16m+15, K = the 4 inputs (lane group 0 only)
-  bf16x4 w2[4][4];  // W2^T tile (rows 16m.., K chunk 16c..)
-  bf16x4 w3[4];     // W3^T rows 0,1 (lanes c < 2), K chunk 16c..
+  bf16x4 w1[4];       // W1^T rows 16m..16m+15, K = the 4 inputs (lane group 0 only)
+  bf16x4 w3[4];       // W3^T rows 0,1 (lanes c < 2), K chunk 16c..
+  const bf16x4 *w2f;  // W2^T fragments in LDS (stage_w2_fragments)
 
   // Fragments from the staged weights (row-major [in][out] bf16).
-  __device__ __forceinline__ void load(const uint16_t *w) {
+  __device__ __forceinline__ void load(const uint16_t *w, const bf16x4 *w2_fragments) {
     const uint32_t lane = threadIdx.x & 63u, g = lane >> 4, c = lane & 15u;
+    w2f = w2_fragments;
     for (int m = 0; m < 4; ++m) {
       for (int j = 0; j < 4; ++j)
         w1[m][j] = g == 0u ? short(w[kOffW1 + j * kHid + 16 * m + c]) : short(0);
-      for (int kc = 0; kc < 4; ++kc)
-        for (int j = 0; j < 4; ++j)
-          w2[m][kc][j] = short(w[kOffW2 + (16 * kc + 4 * g + j) * kHid + 16 * m + c]);
       for (int j = 0; j < 4; ++j)
         w3[m][j] = c < 2u ? short(w[kOffW3 + (16 * m + 4 * g + j) * kOut + c]) : short(0);
     }
@@ -105,28 +124,46 @@ struct MlpPolicy {
     const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
     uint32_t bits = 0u;
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-      // layer-1 input of environment 16t + c, in lane group 0
-      const int src = int(16 * t + c) * 4;
-      uint32_t b01 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(o01)));
-      uint32_t b23 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(o23)));
-      if (g != 0u) b01 = b23 = 0u;
-      const bf16x4 in = as_bf16x4(b01, b23);
-      bf16x4 h1[4], h2[4];
+    for (int tp = 0; tp < 4; tp += 2) {  // tiles tp and tp + 1
+      bf16x4 in[2];
 #pragma unroll
-      for (int m = 0; m < 4; ++m) h1[m] = tanh_bf16(mma(w1[m], in, zero));
+      for (int q = 0; q < 2; ++q) {
+        // layer-1 input of environment 16(tp + q) + c, in lane group 0
+        const int src = int(16 * (tp + q) + c) * 4;
+        uint32_t b01 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(o01)));
+        uint32_t b23 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(o23)));
+        if (g != 0u) b01 = b23 = 0u;
+        in[q] = as_bf16x4(b01, b23);
+      }
+      bf16x4 h1[2][4], h2[2][4];
+#pragma unroll
+      for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int q = 0; q < 2; ++q) h1[q][m] = tanh_bf16(mma(w1[m], in[q], zero));
 #pragma unroll
       for (int m = 0; m < 4; ++m) {
-        f32x4 acc = zero;
+        // an opaque offset keeps the compiler from hoisting the fragment
+        // reads out of the step loop into registers
+        uint32_t off = lane;
+        asm volatile("" : "+v"(off));
+        f32x4 acc[2] = {zero, zero};
 #pragma unroll
-        for (int kc = 0; kc < 4; ++kc) acc = mma(w2[m][kc], h1[kc], acc);
-        h2[m] = tanh_bf16(acc);
+        for (int kc = 0; kc < 4; ++kc) {
+          const bf16x4 wf = w2f[(4 * m + kc) * 64 + off];
+#pragma unroll
+          for (int q = 0; q < 2; ++q) acc[q] = mma(wf, h1[q][kc], acc[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < 2; ++q) h2[q][m] = tanh_bf16(acc[q]);
       }
-      f32x4 logits = zero;
 #pragma unroll
-      for (int kc = 0; kc < 4; ++kc) logits = mma(w3[kc], h2[kc], logits);
-      // rows 0 and 1 of lane c (group 0): the logits of environment 16t + c
-      bits |= (logits[1] > logits[0] ? 1u : 0u) << t;
+      for (int q = 0; q < 2; ++q) {
+        f32x4 logits = zero;
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) logits = mma(w3[kc], h2[q][kc], logits);
+        // rows 0 and 1 of lane c (group 0): the logits of environment 16(tp + q) + c
+        bits |= (logits[1] > logits[0] ? 1u : 0u) << (tp + q);
+      }
     }
     // the environment of lane 16g + c is column c of tile g
     const uint32_t got = uint32_t(__builtin_amdgcn_ds_bpermute(int(c) * 4, int(bits)));
@@ -137,10 +174,13 @@ struct MlpPolicy {
 template <bool kTraj>
 __global__ __launch_bounds__(kResidentBlock) void k_resident_policy(RolloutParams p) {
   __shared__ uint16_t w[kWeights];
+  __shared__ bf16x4 w2f[kW2Frags];
   for (int idx = threadIdx.x; idx < kWeights; idx += kResidentBlock) w[idx] = p.policy_w[idx];
   __syncthreads();
+  stage_w2_fragments(w, w2f);
+  __syncthreads();
   MlpPolicy policy;
-  policy.load(w);
+  policy.load(w, w2f);
   resident_rollout<kTraj>(p, policy);
 }
 
@@ -155,10 +195,13 @@ __global__ __launch_bounds__(kResidentBlock) void k_policy_actions(
     const float *__restrict__ obs, uint32_t n, const uint16_t *__restrict__ policy_w,
     uint8_t *__restrict__ actions) {
   __shared__ uint16_t w[kWeights];
+  __shared__ bf16x4 w2f[kW2Frags];
   for (int idx = threadIdx.x; idx < kWeights; idx += kResidentBlock) w[idx] = policy_w[idx];
   __syncthreads();
+  stage_w2_fragments(w, w2f);
+  __syncthreads();
   MlpPolicy policy;
-  policy.load(w);
+  policy.load(w, w2f);
   for (uint32_t base = blockIdx.x * kResidentBlock; base < n;
        base += gridDim.x * kResidentBlock) {
     const uint32_t i = base + threadIdx.x;
