@@ -96,7 +96,8 @@ def parse():
                                        "resident_f64_1048576x1000", "resident_f16_1048576x1000",
                                        "streaming_16777216x100", "policy_4194304x500",
                                        "policy_separate_4194304x500",
-                                       "policy_two_streams_4194304x500", "copy",
+                                       "policy_two_streams_4194304x500", "horizontal_16x4096",
+                                       "copy",
                                        "valu_reference"],
                     help="run one workload only (for counter collection); prints its JSON")
     return ap.parse_args()
@@ -252,7 +253,69 @@ def bench_configs(cp, only=None):
         res["policy_separate_4194304x500"] = _policy_separate(cp, 1)
     if want("policy_two_streams_4194304x500"):
         res["policy_two_streams_4194304x500"] = _policy_separate(cp, 2)
+    if want("horizontal_16x4096"):
+        res["horizontal_16x4096"] = _horizontal(cp)
     torch.cuda.empty_cache()
+    return res
+
+
+def _horizontal(cp):
+    """Horizontal fusion (the paper's horizontal fusion pass): 16 independent
+    batches of 4,096 environments (own seeds and index ranges), 1,000 steps
+    with obs/reward/done every step, launched from the host one step at a
+    time: one cp_step_group launch per step, against 16 cp_step launches per
+    step, and against one undivided batch of 65,536 environments.  The C
+    entry points are called directly with argument blocks built once (the
+    library advances each handle's step counter in place), so the timing is
+    the library's and the GPU's, not Python's."""
+    import ctypes
+
+    import torch
+
+    k, n, T = 16, 4096, 1000
+    L = cp.lib()
+    members = [cp.CartPoleStates(n, variant=cp.CP_FUSED, env_base=m * n, graphs=False)
+               for m in range(k)]
+    for m, h in enumerate(members):
+        cp.cp_init(h, m)
+    outs = [(torch.empty(4, n, device="cuda"), torch.empty(n, device="cuda"),
+             torch.empty(n, dtype=torch.uint8, device="cuda")) for _ in range(k)]
+    hc = [h.handle() for h in members]
+    ptrs = (ctypes.POINTER(cp.cp_states) * k)(*[ctypes.pointer(h) for h in hc])
+    io = (cp.cp_step_io * k)(*[cp.cp_step_io(None, *[o.data_ptr() for o in out]) for out in outs])
+    whole = cp.CartPoleStates(k * n, variant=cp.CP_FUSED, graphs=False)
+    cp.cp_init(whole, 0)
+    wout = (torch.empty(4, k * n, device="cuda"), torch.empty(k * n, device="cuda"),
+            torch.empty(k * n, dtype=torch.uint8, device="cuda"))
+    wh = whole.handle()
+    wptr = [o.data_ptr() for o in wout]
+
+    def grouped():
+        rc = 0
+        for _ in range(T):
+            rc |= L.cp_step_group(ptrs, io, k)
+        assert rc == 0, cp.lib().cp_last_error()
+
+    def separate():
+        rc = 0
+        for _ in range(T):
+            for h, o in zip(hc, io):
+                rc |= L.cp_step(ctypes.byref(h), None, o.obs, o.reward, o.done)
+        assert rc == 0, cp.lib().cp_last_error()
+
+    def single():
+        rc = 0
+        for _ in range(T):
+            rc |= L.cp_step(ctypes.byref(wh), None, *wptr)
+        assert rc == 0, cp.lib().cp_last_error()
+
+    res = {"members": k, "envs_per_member": n, "steps": T}
+    for name, fn in (("grouped", grouped), ("separate", separate), ("single_batch", single)):
+        fn()  # warm-up
+        wall, ev = timed(fn)
+        res[name] = {"env_steps_per_s": k * n * T / (wall * 1e-3), "us_per_step": wall * 1e3 / T,
+                     "event_us_per_step": ev * 1e3 / T}
+    res["speedup_vs_separate"] = res["separate"]["us_per_step"] / res["grouped"]["us_per_step"]
     return res
 
 

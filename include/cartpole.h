@@ -147,6 +147,31 @@ int cp_init(cp_states *s, uint64_t seed);
  * obs [4][n], reward [n], done [n]: optional outputs for this step.         */
 int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *reward, uint8_t *done);
 
+/* Horizontal fusion (the paper's horizontal fusion pass, Sec. "Fusion
+ * Strategies in XLA": independent computations, of different shapes too,
+ * merged into one kernel so that their launches cost one launch).
+ * cp_step_group performs cp_step(states[m], io[m].actions, io[m].obs,
+ * io[m].reward, io[m].done) for every m < count -- with the same results --
+ * in ONE kernel launch on states[0]->stream, then advances every
+ * states[m]->t by 1.  Members are independent batches: their own arrays,
+ * sizes, seeds, env_base and step counters.  io may be NULL (random
+ * actions, no outputs for every member).
+ * Requirements, checked before any HIP call (on error nothing changes):
+ * 1 <= count <= CP_GROUP_MAX (else CP_ERR_SIZE); every member valid as for
+ * cp_step, binary32, without an MLP policy (else CP_ERR_UNSUPPORTED); all
+ * members on the same stream and no two members sharing any byte of their
+ * state arrays (else CP_ERR_UNSUPPORTED).  Every member is stepped by the
+ * fused step whatever its variant (all levels give the same results); the
+ * call needs no workspace.                                                 */
+#define CP_GROUP_MAX 16
+typedef struct cp_step_io {
+    const uint8_t *actions; /* [n] device, or NULL: random actions           */
+    float *obs;             /* [4][n] or NULL                                */
+    float *reward;          /* [n] or NULL                                   */
+    uint8_t *done;          /* [n] or NULL                                   */
+} cp_step_io;
+int cp_step_group(cp_states *const *states, const cp_step_io *io, int32_t count);
+
 /* n_steps consecutive steps from s->t with random actions from the action
  * stream of `seed` (or the MLP policy when s->policy_w is set), then
  * s->t += n_steps.  n_steps == 0 is a no-op.  Equivalent, bit for bit, to

@@ -44,6 +44,14 @@ class cp_traj(ctypes.Structure):
                 ("total_reward", _p), ("ret_sum", _p), ("global", _p)]
 
 
+class cp_step_io(ctypes.Structure):
+    """One member's inputs and outputs of cp_step_group (cartpole.h)."""
+    _fields_ = [("actions", _p), ("obs", _p), ("reward", _p), ("done", _p)]
+
+
+CP_GROUP_MAX = 16
+
+
 class CartPoleError(RuntimeError):
     def __init__(self, code, message):
         super().__init__(f"cartpole error {code}: {message}")
@@ -65,6 +73,8 @@ def lib():
         L.cp_init.argtypes = [P(cp_states), ctypes.c_uint64]
         L.cp_step.argtypes = [P(cp_states), _p, _p, _p, _p]
         L.cp_rollout.argtypes = [P(cp_states), ctypes.c_int64, ctypes.c_uint64, P(cp_traj)]
+        L.cp_step_group.argtypes = [P(P(cp_states)), P(cp_step_io), ctypes.c_int32]
+        L.cp_step_group.restype = ctypes.c_int
         L.cp_policy.argtypes = [_p, ctypes.c_int64, _p, _p, _p]
         L.cp_policy.restype = ctypes.c_int
         L.cp_workspace_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32]
@@ -165,6 +175,23 @@ def cp_step(states: CartPoleStates, actions=None, obs=None, reward=None, done=No
     h = states.handle()
     _check(lib().cp_step(ctypes.byref(h), _ptr(actions), _ptr(obs), _ptr(reward), _ptr(done)))
     states._sync_back(h)
+
+
+def cp_step_group(members, ios=None) -> None:
+    """One step of every CartPoleStates in `members` (at most CP_GROUP_MAX)
+    in one kernel launch, with the results of cp_step on each.  ios: None
+    (random actions, no outputs), or per member a tuple (actions, obs, reward,
+    done) whose entries may be None."""
+    hs = [m.handle() for m in members]
+    k = len(hs)
+    ptrs = (ctypes.POINTER(cp_states) * max(k, 1))(*[ctypes.pointer(h) for h in hs])
+    io = None
+    if ios is not None:
+        assert len(ios) == k
+        io = (cp_step_io * max(k, 1))(*[cp_step_io(*[_ptr(t) for t in e]) for e in ios])
+    _check(lib().cp_step_group(ptrs, io, k))
+    for m, h in zip(members, hs):
+        m._sync_back(h)
 
 
 def cp_rollout(states: CartPoleStates, n_steps: int, seed: int, traj: Trajectory = None) -> None:

@@ -190,6 +190,71 @@ CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *rewa
   return ok();
 }
 
+namespace {
+
+// Byte ranges of a member's state arrays (for the no-sharing check).
+struct Span {
+  uintptr_t lo, hi;
+};
+
+int state_spans(const cp_states *s, Span out[6]) {
+  const uintptr_t n = uintptr_t(s->n), eb = elem_bytes(s->precision);
+  const void *a[6] = {s->x, s->x_dot, s->theta, s->theta_dot, s->ep_index, s->ep_len};
+  const uintptr_t b[6] = {eb, eb, eb, eb, 4u, 4u};
+  for (int j = 0; j < 6; ++j) {
+    out[j].lo = reinterpret_cast<uintptr_t>(a[j]);
+    out[j].hi = out[j].lo + n * b[j];
+  }
+  return 6;
+}
+
+}  // namespace
+
+CP_API int cp_step_group(cp_states *const *states, const cp_step_io *io, int32_t count) {
+  if (!states) return fail(CP_ERR_NULL, "states is NULL");
+  if (count < 1 || count > int32_t(cp::kGroupMax))
+    return fail(CP_ERR_SIZE, "count = %d is outside [1, %u]", (int)count, cp::kGroupMax);
+  static_assert(CP_GROUP_MAX == cp::kGroupMax, "group size");
+  Span spans[cp::kGroupMax][6];
+  for (int32_t m = 0; m < count; ++m) {
+    const cp_states *s = states[m];
+    if (int e = check_states(s)) return e;
+    if (int e = check_steps(s, 1)) return e;
+    if (s->precision != CP_PREC_F32)
+      return fail(CP_ERR_UNSUPPORTED, "member %d: group steps are binary32 only", (int)m);
+    if (s->policy_w)
+      return fail(CP_ERR_UNSUPPORTED, "member %d: the MLP policy runs in CP_RESIDENT only", (int)m);
+    if (s->stream != states[0]->stream)
+      return fail(CP_ERR_UNSUPPORTED, "member %d is on another stream than member 0", (int)m);
+    if (io && ((io[m].obs && !aligned4(io[m].obs)) || (io[m].reward && !aligned4(io[m].reward))))
+      return fail(CP_ERR_ALIGN, "member %d: obs and reward must be 4-byte aligned", (int)m);
+    state_spans(s, spans[m]);
+    for (int32_t q = 0; q < m; ++q)
+      for (int j = 0; j < 6; ++j)
+        for (int k = 0; k < 6; ++k)
+          if (spans[m][j].lo < spans[q][k].hi && spans[q][k].lo < spans[m][j].hi)
+            return fail(CP_ERR_UNSUPPORTED, "members %d and %d share state memory", (int)q,
+                        (int)m);
+  }
+  cp::GroupParams g{};
+  g.count = uint32_t(count);
+  for (int32_t m = 0; m < count; ++m) {
+    const cp_states *s = states[m];
+    cp::StepParams p = step_params(s, s->seed);
+    if (io) {
+      p.actions = io[m].actions;
+      p.obs = io[m].obs;
+      p.reward = io[m].reward;
+      p.done = io[m].done;
+    }
+    g.p[m] = p;
+  }
+  const hipError_t err = cp::launch_group_step(g, static_cast<hipStream_t>(states[0]->stream));
+  if (int e = hip_status(err, "cp_step_group launch")) return e;
+  for (int32_t m = 0; m < count; ++m) states[m]->t += 1;
+  return ok();
+}
+
 CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj) {
   if (int e = check_states(s)) return e;
   if (n_steps < 0) return fail(CP_ERR_SIZE, "n_steps = %lld is negative", (long long)n_steps);

@@ -100,6 +100,21 @@ hipError_t launch_episode_sums(const uint32_t *ep_index, const uint32_t *ep_len,
                                bool after, unsigned long long extra, unsigned long long *global,
                                hipStream_t stream);
 
+// Horizontal fusion: one launch steps up to kGroupMax independent batches
+// (their own arrays, sizes, seeds and step indices), block ranges assigned
+// to the members in order: member m owns blocks [first_block[m],
+// first_block[m + 1]); first_block[count] is the grid size and the entries
+// after it are 0xFFFFFFFF.  The whole table travels in the kernel arguments.
+constexpr uint32_t kGroupMax = 16;
+struct GroupParams {
+  uint32_t count;
+  uint32_t first_block[kGroupMax + 1];
+  StepParams p[kGroupMax];
+};
+static_assert(sizeof(GroupParams) <= 4096, "kernel arguments are limited to 4 KiB");
+// Fills first_block from the members' sizes (g.count and g.p[0..count) set).
+hipError_t launch_group_step(GroupParams g, hipStream_t stream);
+
 // Concatenated-state level: two kernels per step around an [n][4] array
 // (16 bytes per environment of workspace, 16-byte aligned).
 size_t concat_workspace_bytes(uint32_t n);

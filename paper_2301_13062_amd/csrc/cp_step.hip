@@ -190,6 +190,28 @@ __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   if (i < p.n) fused_one<kExplicit, kEager, kStream>(p, i, a);
 }
 
+// Horizontal fusion (the paper's horizontal fusion pass, Sec. "Fusion
+// Strategies in XLA"): independent batches of different sizes stepped by one
+// launch.  Each block finds its member with a scalar scan of the block
+// prefix table (in the kernel arguments; entries past the last member hold
+// the largest index, so the scan has a fixed length and one batched load)
+// and runs the fused step of that member's environment: the results are
+// those of a cp_step on each member.
+__global__ __launch_bounds__(kBlock) void k_group_step(GroupParams g) {
+  uint32_t m = 0;
+#pragma unroll
+  for (uint32_t j = 1; j < kGroupMax; ++j) m += blockIdx.x >= g.first_block[j] ? 1u : 0u;
+  const StepParams &p = g.p[m];
+  const uint32_t i = (blockIdx.x - g.first_block[m]) * kBlock + threadIdx.x;
+  if (p.actions) {
+    if (i < p.n) fused_one<true, true>(p, i, 0u);
+  } else {
+    // random actions: one block per wave, before any lane leaves
+    const uint32_t a = action_bit_wave(p.kact, p.env_base + i, p.t);
+    if (i < p.n) fused_one<false, true>(p, i, a);
+  }
+}
+
 // Graph replay of fused rollouts.  Launched one by one, a latency-bound
 // step costs the host more than the GPU; a graph hands the GPU all steps of
 // a rollout at once.  Its launches cannot change their arguments from
@@ -412,6 +434,17 @@ hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
   } else {
     hipLaunchKernelGGL((k_fused_step<false, false>), g, b, 0, stream, p);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_group_step(GroupParams g, hipStream_t stream) {
+  uint32_t blocks = 0;
+  for (uint32_t m = 0; m < g.count; ++m) {
+    g.first_block[m] = blocks;
+    blocks += (g.p[m].n + kBlock - 1u) / kBlock;
+  }
+  for (uint32_t m = g.count; m <= kGroupMax; ++m) g.first_block[m] = m == g.count ? blocks : ~0u;
+  hipLaunchKernelGGL(k_group_step, dim3(blocks), dim3(kBlock), 0, stream, g);
   return hipGetLastError();
 }
 

@@ -218,3 +218,69 @@ def test_policy_alone_validation():
     assert L.cp_policy(A, 2 ** 31, A, A, None) == cp.CP_ERR_SIZE
     assert L.cp_policy(A + 2, 10, A, A, None) == cp.CP_ERR_ALIGN
     assert L.cp_policy(A, 10, A + 1, A, None) == cp.CP_ERR_ALIGN
+
+
+# --------------------------------------------------------------------------- cp_step_group
+def member(base, **kw):
+    h = cp.cp_states(base, base + 0x1000, base + 0x2000, base + 0x3000, base + 0x4000,
+                     base + 0x5000, 1000, 0, cp.CP_FUSED, 123, 7, None, None, None, 0)
+    for k, v in kw.items():
+        setattr(h, k, v)
+    return h
+
+
+def call_group(hs, io=None, count=None):
+    arr = (ctypes.POINTER(cp.cp_states) * max(len(hs), 1))(*[ctypes.pointer(h) for h in hs])
+    return cp.lib().cp_step_group(arr, io, len(hs) if count is None else count)
+
+
+def members(k):
+    return [member(A + 0x10000 * m) for m in range(k)]
+
+
+@pytest.mark.parametrize("count", [0, -1, 17])
+def test_group_count_out_of_range(count):
+    hs = members(17)
+    assert call_group(hs, count=count) == cp.CP_ERR_SIZE
+    assert all(h.t == 7 for h in hs)
+
+
+def test_group_null_states():
+    assert cp.lib().cp_step_group(None, None, 1) == cp.CP_ERR_NULL
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(x=None), cp.CP_ERR_NULL),
+    (dict(n=0), cp.CP_ERR_SIZE),
+    (dict(precision=cp.CP_PREC_F64), cp.CP_ERR_UNSUPPORTED),
+    (dict(policy_w=A + 0x900000), cp.CP_ERR_UNSUPPORTED),
+    (dict(stream=0x1234), cp.CP_ERR_UNSUPPORTED),
+    (dict(t=(1 << 31) - 1), cp.CP_ERR_RANGE),
+    (dict(x=MIS), cp.CP_ERR_ALIGN),
+])
+def test_group_rejects_a_bad_member(bad, code):
+    hs = members(3)
+    for k, v in bad.items():
+        setattr(hs[2], k, v)
+    t_before = [h.t for h in hs]
+    assert call_group(hs) == code
+    assert [h.t for h in hs] == t_before  # nothing advanced
+    assert cp.lib().cp_last_error()
+
+
+@pytest.mark.parametrize("shift", [0, 0x800, 0x5000 - 4])
+def test_group_rejects_members_sharing_state_memory(shift):
+    # the same handle twice, or a second member whose arrays overlap the
+    # first member's (shift 0x5000 - 4: its x overlaps the first's ep_len)
+    a = member(A)
+    b = member(A + shift)
+    assert call_group([a, b]) == cp.CP_ERR_UNSUPPORTED
+    assert "share state memory" in cp.lib().cp_last_error().decode()
+    assert a.t == 7 and b.t == 7
+
+
+def test_group_rejects_misaligned_outputs():
+    hs = members(2)
+    io = (cp.cp_step_io * 2)(cp.cp_step_io(None, A + 0x800000, None, None),
+                             cp.cp_step_io(None, MIS + 0x800000, None, None))
+    assert call_group(hs, io=io) == cp.CP_ERR_ALIGN
