@@ -192,7 +192,8 @@ def bench_copy():
             "GB_per_s": 2 * (1 << 30) / (ev / 5 * 1e-3) / 1e9}
 
 
-VALU_REFERENCE_FORMS = ("fma_f32_vgpr", "fma_f32_sgpr_operand", "rotate_u32", "rcp_f32")
+VALU_REFERENCE_FORMS = ("fma_f32_vgpr", "fma_f32_sgpr_operand", "rotate_u32", "rcp_f32", "fma_f64",
+                        "rcp_f64", "pk_fma_f16", "fma_f16", "mul_f16")
 
 
 def bench_valu_reference():
@@ -200,7 +201,9 @@ def bench_valu_reference():
     class: eight independent chains of one form per lane, eight waves per
     SIMD, no memory traffic (reference kernels in their own library).  Forms:
     binary32 FMA on vector registers; the same with a wave-uniform scalar
-    operand; a 32-bit rotation (the generator's); the binary32 reciprocal.
+    operand; a 32-bit rotation (the generator's); the binary32 reciprocal;
+    binary64 FMA and reciprocal; packed (two per lane) and single binary16
+    FMA; single binary16 multiply.
     They are the practical ceilings for the VALU-bound kernels' instruction
     mixes; the FMA form is also given as a fraction of the op-rate peak."""
     import ctypes

@@ -50,15 +50,72 @@ __device__ __forceinline__ double reset_value64(uint32_t h16) {
   return double(int32_t(h16) - int32_t(1 << 15)) * kResetScale64;
 }
 
+// binary64 sin and cos on |th| <= 1/4 (every angle a non-terminated state
+// holds): Taylor polynomials through th^13 and th^12, whose first omitted
+// terms are below 2^-64 relative, so the results are within about half an
+// ulp plus the rounding of the evaluation; the library routines beyond.
+__device__ __forceinline__ double sin_small64(double th) {
+  const double z = th * th;
+  double p = 1.0 / 6227020800.0;               //  1/13!
+  p = __builtin_fma(p, z, -1.0 / 39916800.0);  // -1/11!
+  p = __builtin_fma(p, z, 1.0 / 362880.0);     //  1/9!
+  p = __builtin_fma(p, z, -1.0 / 5040.0);      // -1/7!
+  p = __builtin_fma(p, z, 1.0 / 120.0);        //  1/5!
+  p = __builtin_fma(p, z, -1.0 / 6.0);         // -1/3!
+  return __builtin_fma(th * z, p, th);
+}
+
+__device__ __forceinline__ double cos_small64(double th) {
+  const double z = th * th;
+  double q = 1.0 / 479001600.0;                //  1/12!
+  q = __builtin_fma(q, z, -1.0 / 3628800.0);   // -1/10!
+  q = __builtin_fma(q, z, 1.0 / 40320.0);      //  1/8!
+  q = __builtin_fma(q, z, -1.0 / 720.0);       // -1/6!
+  q = __builtin_fma(q, z, 1.0 / 24.0);         //  1/4!
+  q = __builtin_fma(q, z, -0.5);               // -1/2!
+  return __builtin_fma(z, q, 1.0);
+}
+
+// Both at once.  Per lane the choice depends on the lane's own angle only
+// (so results do not depend on which environments share a wave); when every
+// lane of the wave holds a small angle one uniform branch skips the library
+// routines.
+__device__ __forceinline__ void sincos64(double th, double &sn, double &c) {
+  if (__all(__builtin_fabs(th) <= 0.25)) {
+    sn = sin_small64(th);
+    c = cos_small64(th);
+  } else {
+    const bool small = __builtin_fabs(th) <= 0.25;
+    sn = small ? sin_small64(th) : sin(th);
+    c = small ? cos_small64(th) : cos(th);
+  }
+}
+
+// Division by the total mass M = 1.1 (binary64): the product with the
+// rounded reciprocal, corrected once with the exact residual.  By
+// Markstein's theorem (a reciprocal within half an ulp and a quotient
+// within one ulp give, after one fused correction, the rounded quotient)
+// this is the correctly rounded x / M whenever nothing underflows, i.e. for
+// |x| above about 2^-960; the binary64 step's dividends are of order 1e-3..10.
+constexpr double kTotalMass64 = 0.1 + 1.0;
+constexpr double kInvTotalMass64 = 1.0 / kTotalMass64;
+
+__device__ __forceinline__ double div_mass64(double x) {
+  const double q = x * kInvTotalMass64;
+  const double r = __builtin_fma(-q, kTotalMass64, x);
+  return __builtin_fma(r, kInvTotalMass64, q);
+}
+
 __device__ __forceinline__ State64 dynamics64(const State64 &s, double force) {
-  const double g = 9.8, mc = 1.0, mp = 0.1, l = 0.5, tau = 0.02;
-  const double m = mp + mc, pml = mp * l, four3 = 4.0 / 3.0;
-  const double c = cos(s.th), sn = sin(s.th);
+  const double g = 9.8, mp = 0.1, l = 0.5, tau = 0.02;
+  const double pml = mp * l, four3 = 4.0 / 3.0;
+  double sn, c;
+  sincos64(s.th, sn, c);
   const double thd2 = s.thd * s.thd;
   const double c2 = c * c;
-  const double temp = (force + pml * thd2 * sn) / m;
-  const double thacc = (g * sn - c * temp) / (l * (four3 - mp * c2 / m));
-  const double xacc = temp - pml * thacc * c / m;
+  const double temp = div_mass64(force + pml * thd2 * sn);
+  const double thacc = (g * sn - c * temp) / (l * (four3 - div_mass64(mp * c2)));
+  const double xacc = temp - div_mass64(pml * thacc * c);
   return State64{s.x + tau * s.xd, s.xd + tau * xacc, s.th + tau * s.thd, s.thd + tau * thacc};
 }
 
