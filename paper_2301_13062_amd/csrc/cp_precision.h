@@ -189,9 +189,10 @@ __device__ __forceinline__ void sincos16(half_t th, half_t &sn, half_t &c) {
   sn = to_half(sf);
   c = to_half(cf);
   if (near_f16_midpoint(sf) || near_f16_midpoint(cf)) {
-    const double thd = double(th);
-    sn = half_t(float(nearest_f16(sin(thd))));
-    c = half_t(float(nearest_f16(cos(thd))));
+    double sd, cd;
+    sincos64(double(th), sd, cd);
+    sn = half_t(float(nearest_f16(sd)));
+    c = half_t(float(nearest_f16(cd)));
   }
 }
 
