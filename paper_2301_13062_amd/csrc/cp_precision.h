@@ -158,6 +158,20 @@ __device__ __forceinline__ half_t div16(half_t a, half_t b) {
   return to_half(div_rn(float(a), float(b)));
 }
 
+// a / m for the binary16 total mass m = RN16(RN16(0.1) + 1) = 1.099609375:
+// the binary32 product with RN32(1/m) corrected once with the exact residual,
+// then rounded once to binary16.  For every binary16 dividend this is the
+// binary16 value nearest to the exact quotient (checked exhaustively).
+constexpr float kTotalMass16 = 1.099609375f;
+constexpr float kInvTotalMass16 = 1.0f / kTotalMass16;
+
+__device__ __forceinline__ half_t div16_mass(half_t a) {
+  const float x = float(a);
+  const float q = x * kInvTotalMass16;
+  const float r = __builtin_fmaf(-q, kTotalMass16, x);
+  return to_half(__builtin_fmaf(r, kInvTotalMass16, q));
+}
+
 // The binary16 value nearest to v (ties to even), computed exactly in
 // binary64: scaling by powers of two is exact and rint rounds to nearest
 // even.  Quantum 2^(e-11) for |v| in [2^(e-1), 2^e), at least 2^-24.
@@ -197,16 +211,16 @@ __device__ __forceinline__ void sincos16(half_t th, half_t &sn, half_t &c) {
 }
 
 __device__ __forceinline__ State16 dynamics16(const State16 &s, half_t force) {
-  const half_t g = half_t(9.8), mc = half_t(1.0), mp = half_t(0.1), l = half_t(0.5);
+  const half_t g = half_t(9.8), mp = half_t(0.1), l = half_t(0.5);
   const half_t tau = half_t(0.02), four3 = half_t(4.0 / 3.0);
-  const half_t m = mp + mc, pml = mp * l;
+  const half_t pml = mp * l;  // the total mass RN16(mp + mc) is kTotalMass16
   half_t sn, c;
   sincos16(s.th, sn, c);
   const half_t thd2 = s.thd * s.thd;
   const half_t c2 = c * c;
-  const half_t temp = div16(force + pml * thd2 * sn, m);
-  const half_t thacc = div16(g * sn - c * temp, l * (four3 - div16(mp * c2, m)));
-  const half_t xacc = temp - div16(pml * thacc * c, m);
+  const half_t temp = div16_mass(force + pml * thd2 * sn);
+  const half_t thacc = div16(g * sn - c * temp, l * (four3 - div16_mass(mp * c2)));
+  const half_t xacc = temp - div16_mass(pml * thacc * c);
   return State16{s.x + tau * s.xd, s.xd + tau * xacc, s.th + tau * s.thd, s.thd + tau * thacc};
 }
 
