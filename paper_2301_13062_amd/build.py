@@ -14,6 +14,11 @@ SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip"]
 # of its own that only the benchmark loads.
 REF_SOURCES = ["ref_valu.hip"]
 REF_LIB = os.path.join(OUT_DIR, "libcpref.so")
+# A plain C client of the ABI (cartpole.h and the HIP runtime API only), built
+# with the host C compiler; the GPU tests run it.
+CLIENT_SRC = os.path.join(ROOT, "tests", "capi_client.c")
+CLIENT = os.path.join(OUT_DIR, "capi_client")
+ROCM = os.environ.get("ROCM_PATH", "/opt/rocm")
 
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
@@ -42,10 +47,24 @@ def _hipcc(sources, out, verbose):
     os.replace(tmp, out)
 
 
+def _client(verbose):
+    tmp = CLIENT + ".tmp"
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+           f"-I{ROCM}/include", f"-I{INCLUDE}", CLIENT_SRC, f"-L{ROCM}/lib", "-lamdhip64",
+           f"-L{OUT_DIR}", "-lcartpole", f"-Wl,-rpath,{ROCM}/lib", "-Wl,-rpath,$ORIGIN", "-o", tmp]
+    if verbose:
+        print(" ".join(cmd))
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"gcc failed:\n{r.stderr}")
+    os.replace(tmp, CLIENT)
+
+
 def build(verbose=False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
     _hipcc(SOURCES, LIB, verbose)
     _hipcc(REF_SOURCES, REF_LIB, verbose)
+    _client(verbose)
     return LIB
 
 

@@ -284,3 +284,14 @@ def test_group_rejects_misaligned_outputs():
     io = (cp.cp_step_io * 2)(cp.cp_step_io(None, A + 0x800000, None, None),
                              cp.cp_step_io(None, MIS + 0x800000, None, None))
     assert call_group(hs, io=io) == cp.CP_ERR_ALIGN
+
+
+def test_plain_c_client_is_built_and_links():
+    # the C client of the ABI (run by the GPU tests) resolves the library
+    # next to it and the HIP runtime, with no Python involved
+    from paper_2301_13062_amd import build as B
+
+    assert os.path.exists(B.CLIENT)
+    out = subprocess.run(["ldd", B.CLIENT], capture_output=True, text=True, check=True).stdout
+    lib = [ln for ln in out.splitlines() if "libcartpole.so" in ln]
+    assert lib and "not found" not in lib[0] and os.path.dirname(B.CLIENT) in lib[0], out
