@@ -101,7 +101,7 @@ def parse():
                                        "policy_separate_4194304x500",
                                        "policy_two_streams_4194304x500", "horizontal_16x4096",
                                        "copy",
-                                       "valu_reference"],
+                                       "valu_reference", "graph_floor"],
                     help="run one workload only (for counter collection); prints its JSON")
     return ap.parse_args()
 
@@ -235,6 +235,53 @@ def bench_valu_reference():
     fma = res["fma_f32_vgpr"]["wave64_per_cu_per_ns"] * 256e9 * 64
     res["fma_f32_vgpr"].update({"lane_ops_per_s": fma,
                                 "frac_of_op_peak": fma / (VALU_PEAK_TOPS * 1e12)})
+    return res
+
+
+def bench_graph_floor(head_us=None):
+    """Floors for one launch per step replayed from a HIP graph (the
+    headline's regime), from reference kernels in their own library: an
+    empty kernel (the graph's per-node cost) and a kernel that moves exactly
+    the headline step's 61 bytes per environment for 65,536 environments
+    with no arithmetic (the memory round trip), each captured 1,000 times
+    into a graph and replayed."""
+    import ctypes
+
+    import torch
+
+    from paper_2301_13062_amd import build as B
+
+    ref = ctypes.CDLL(B.REF_LIB)
+    ref.cpref_empty.argtypes = [ctypes.c_int, ctypes.c_void_p]
+    ref.cpref_touch.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_int64, ctypes.c_void_p]
+    n, K = 65536, 1000
+    f = [torch.zeros(n, device="cuda") for _ in range(4)]
+    ln = torch.zeros(n, dtype=torch.int32, device="cuda")
+    obs = torch.empty(4, n, device="cuda")
+    rew = torch.empty(n, device="cuda")
+    done = torch.empty(n, dtype=torch.uint8, device="cuda")
+    ptrs = [t.data_ptr() for t in f] + [ln.data_ptr(), obs.data_ptr(), rew.data_ptr(),
+                                       done.data_ptr()]
+    res = {}
+    for name, launch in (("empty_kernel", lambda st: ref.cpref_empty(n // 256, st)),
+                         ("touch_61B_per_env", lambda st: ref.cpref_touch(*ptrs, n, st))):
+        g = torch.cuda.CUDAGraph()
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            launch(side.cuda_stream)  # warm-up outside capture
+        torch.cuda.current_stream().wait_stream(side)
+        with torch.cuda.graph(g):
+            st = torch.cuda.current_stream().cuda_stream
+            for _ in range(K):
+                if launch(st) != 0:
+                    raise RuntimeError("reference kernel failed to launch")
+        g.replay()
+        wall, ev = timed(g.replay, reps=3)
+        res[name] = {"us_per_node": ev * 1e3 / (3 * K)}
+    if head_us is not None:
+        res["headline_us_per_step"] = head_us
+        res["headline_over_touch"] = head_us / res["touch_61B_per_env"]["us_per_node"]
     return res
 
 
@@ -581,7 +628,8 @@ def main():
         print(json.dumps({"only": "headline", **head["fused"]}))
         return
     if args.only:
-        refs = {"copy": bench_copy, "valu_reference": bench_valu_reference}
+        refs = {"copy": bench_copy, "valu_reference": bench_valu_reference,
+                "graph_floor": bench_graph_floor}
         res = refs[args.only]() if args.only in refs else bench_configs(cp, args.only)[args.only]
         print(json.dumps({"only": args.only, **res}))
         return
@@ -624,7 +672,8 @@ def main():
     if not args.quick:
         line["configs"] = bench_configs(cp)
         line["unroll"] = bench_unroll(cp)
-        line["references"] = {"copy": bench_copy(), "valu": bench_valu_reference()}
+        line["references"] = {"copy": bench_copy(), "valu": bench_valu_reference(),
+                              "graph_floor": bench_graph_floor(kern_us)}
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline()
         if not args.quick:

@@ -10,9 +10,9 @@ OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(OUT_DIR, "libcartpole.so")
 
 SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip"]
-# A measurement reference (the sustained vector-FMA issue rate), in a library
-# of its own that only the benchmark loads.
-REF_SOURCES = ["ref_valu.hip"]
+# Measurement references (issue rates by instruction class, per-launch floors
+# of graph replay), in a library of their own that only the benchmark loads.
+REF_SOURCES = ["ref_valu.hip", "ref_latency.hip"]
 REF_LIB = os.path.join(OUT_DIR, "libcpref.so")
 # A plain C client of the ABI (cartpole.h and the HIP runtime API only), built
 # with the host C compiler; the GPU tests run it.

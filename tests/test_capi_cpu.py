@@ -43,7 +43,8 @@ def test_reference_library_is_separate():
 
     out = subprocess.run(["nm", "-D", "--defined-only", B.REF_LIB], capture_output=True,
                          text=True, check=True).stdout
-    assert sorted(set(re.findall(r"\bT (\w+)", out))) == ["cpref_chains", "cpref_ops_per_iter"]
+    assert sorted(set(re.findall(r"\bT (\w+)", out))) == ["cpref_chains", "cpref_empty",
+                                                            "cpref_ops_per_iter", "cpref_touch"]
     main = subprocess.run(["nm", "-D", cp.LIB_PATH], capture_output=True, text=True).stdout
     assert "cpref_" not in main
 
