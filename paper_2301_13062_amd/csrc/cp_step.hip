@@ -29,6 +29,10 @@ constexpr int kBlock = 256;
 // from it on the bandwidth-oriented one, which touches the episode index
 // only on termination.
 constexpr uint32_t kEagerMaxEnvs = kObsStateMinEnvs;
+// Below this batch size every byte offset of a fused step fits in 32 bits:
+// at most 4 bytes per environment from an array's base (or an obs plane's).
+constexpr uint32_t kOff32MaxEnvs = 1u << 30;
+static_assert(kEagerMaxEnvs <= kOff32MaxEnvs, "the latency-oriented step uses 32-bit offsets");
 
 // Accesses through pointers that the compiler cannot place in global memory
 // by itself (pointers loaded from memory rather than passed as kernel
@@ -37,19 +41,23 @@ constexpr uint32_t kEagerMaxEnvs = kObsStateMinEnvs;
 template <class T>
 using global_ptr = __attribute__((address_space(1))) T *;
 
-template <class T>
-__device__ __forceinline__ void st_global(T *base, size_t i, T v) {
-  ((global_ptr<T>)base)[i] = v;
-}
-
-template <class T>
-__device__ __forceinline__ void st_global_nt(T *base, size_t i, T v) {
-  __builtin_nontemporal_store(v, (global_ptr<T>)base + i);
-}
-
-template <class T>
-__device__ __forceinline__ T ld_global(const T *base, size_t i) {
-  return ((global_ptr<const T>)base)[i];
+// Element i of a global array.  kOff32: the caller guarantees that the byte
+// offset i * sizeof(T) fits in 32 bits, and the access takes the array's
+// scalar base plus a 32-bit vector offset instead of a 64-bit vector address
+// computed per array (in the one-step-per-launch step, where one wave per
+// SIMD runs its instructions back to back, that 64-bit arithmetic cost 12%
+// of the step).  The offset passes an empty volatile asm at each use so that
+// the compiler widens it next to the access, where the scalar-base form is
+// selected, rather than once for all accesses and then adds it to each base
+// in 64-bit vector arithmetic.
+template <bool kOff32, class T>
+__device__ __forceinline__ global_ptr<T> elem(T *base, uint32_t i) {
+  if (kOff32) {
+    uint32_t off = i * uint32_t(sizeof(T));
+    asm volatile("" : "+v"(off));
+    return (global_ptr<T>)((__attribute__((address_space(1))) char *)base + off);
+  }
+  return (global_ptr<T>)base + i;
 }
 
 
@@ -74,29 +82,38 @@ __global__ __launch_bounds__(kBlock) void k_init(typename P::T *__restrict__ x,
 
 // Stores of one environment's step: the state (unless the trajectory's obs
 // plane holds it), the running episode length, the step outputs and the
-// rollout accumulators.
+// rollout accumulators.  kOff32: as for elem(), for every array written
+// (each obs plane addressed from its own base).
+template <bool kOff32 = false>
 __device__ __forceinline__ void store_step(const StepParams &p, uint32_t i, const State &o,
                                            uint32_t len, uint32_t d, uint32_t ret) {
   if (p.x) {
-    st_global(p.x, i, o.x);
-    st_global(p.xd, i, o.xd);
-    st_global(p.th, i, o.th);
-    st_global(p.thd, i, o.thd);
+    *elem<kOff32>(p.x, i) = o.x;
+    *elem<kOff32>(p.xd, i) = o.xd;
+    *elem<kOff32>(p.th, i) = o.th;
+    *elem<kOff32>(p.thd, i) = o.thd;
   }
-  st_global(p.ep_len, i, len);
+  *elem<kOff32>(p.ep_len, i) = len;
   if (p.obs) {
-    st_global_nt(p.obs, i, o.x);
-    st_global_nt(p.obs, p.n + i, o.xd);
-    st_global_nt(p.obs, 2u * p.n + i, o.th);
-    st_global_nt(p.obs, 3u * p.n + i, o.thd);
+    __builtin_nontemporal_store(o.x, elem<kOff32>(p.obs, i));
+    __builtin_nontemporal_store(o.xd, elem<kOff32>(p.obs + size_t(p.n), i));
+    __builtin_nontemporal_store(o.th, elem<kOff32>(p.obs + 2u * size_t(p.n), i));
+    __builtin_nontemporal_store(o.thd, elem<kOff32>(p.obs + 3u * size_t(p.n), i));
   }
-  if (p.reward) st_global_nt(p.reward, i, 1.0f);
-  if (p.done) st_global_nt(p.done, i, uint8_t(d));
-  if (p.done_count)
-    st_global(p.done_count, i, (p.first ? 0u : ld_global(p.done_count, i)) + d);
-  if (p.total_reward)
-    st_global(p.total_reward, i, (p.first ? 0.0f : ld_global(p.total_reward, i)) + 1.0f);
-  if (p.ret_sum) st_global(p.ret_sum, i, (p.first ? 0u : ld_global(p.ret_sum, i)) + ret);
+  if (p.reward) __builtin_nontemporal_store(1.0f, elem<kOff32>(p.reward, i));
+  if (p.done) __builtin_nontemporal_store(uint8_t(d), elem<kOff32>(p.done, i));
+  if (p.done_count) {
+    auto q = elem<kOff32>(p.done_count, i);
+    *q = (p.first ? 0u : *q) + d;
+  }
+  if (p.total_reward) {
+    auto q = elem<kOff32>(p.total_reward, i);
+    *q = (p.first ? 0.0f : *q) + 1.0f;
+  }
+  if (p.ret_sum) {
+    auto q = elem<kOff32>(p.ret_sum, i);
+    *q = (p.first ? 0u : *q) + ret;
+  }
 }
 
 // The fused step of one environment after its loads: s, its running
@@ -104,30 +121,45 @@ __device__ __forceinline__ void store_step(const StepParams &p, uint32_t i, cons
 // where a step is latency-bound): the episode index was loaded with the
 // state and the next start state is drawn while the dynamics run, instead of
 // a second memory round trip and the draw after the termination test; the
-// episode index is still written only on termination.
-template <bool kEager>
+// episode index is still written only on termination.  kOff32: as for
+// elem(), for every array the step touches.
+template <bool kEager, bool kOff32>
 __device__ __forceinline__ void fused_rest(const StepParams &p, uint32_t i, uint32_t a,
                                            const State &s, uint32_t len0, uint32_t k0) {
   const uint32_t env = p.env_base + i;
   uint32_t len = len0 + 1u, ret = 0u, k = 0u;
-  State r{0.f, 0.f, 0.f, 0.f};
   if (kEager) {
+    // Both candidates for every lane, then a select, no branch: left to
+    // itself the compiler sinks the draw into a branch for the terminated
+    // lanes, run after the dynamics and behind a second load of its key from
+    // the kernel arguments (the opaque register constraint prevents that;
+    // measured 1% faster).
     k = k0 + 1u;
-    r = reset_draw(p.krst, env, k);
+    State o = dynamics(s, force_of(a));
+    State r = reset_draw(p.krst, env, k);
+    asm volatile("" : "+v"(r.x), "+v"(r.xd), "+v"(r.th), "+v"(r.thd));
+    const bool d = terminated(o);
+    o.x = d ? r.x : o.x;
+    o.xd = d ? r.xd : o.xd;
+    o.th = d ? r.th : o.th;
+    o.thd = d ? r.thd : o.thd;
+    ret = d ? len : 0u;
+    len = d ? 0u : len;
+    if (d) *elem<kOff32>(p.ep_index, i) = k;
+    store_step<kOff32>(p, i, o, len, d ? 1u : 0u, ret);
+    return;
   }
   State o = dynamics(s, force_of(a));
   const uint32_t d = terminated(o) ? 1u : 0u;
   if (d) {
     ret = len;
     len = 0u;
-    if (!kEager) {
-      k = p.ep_index[i] + 1u;
-      r = reset_draw(p.krst, env, k);
-    }
-    p.ep_index[i] = k;
-    o = r;
+    const auto q = elem<kOff32>(p.ep_index, i);
+    k = *q + 1u;
+    *q = k;
+    o = reset_draw(p.krst, env, k);
   }
-  store_step(p, i, o, len, d, ret);
+  store_step<kOff32>(p, i, o, len, d, ret);
 }
 
 // kStream: the step reads its state from other arrays than it writes (the
@@ -135,16 +167,20 @@ __device__ __forceinline__ void fused_rest(const StepParams &p, uint32_t i, uint
 // non-temporal loads keep those lines out of the caches (measured: 135 ->
 // 129 us per launch at 16,777,216 environments, while for a step that
 // rewrites the arrays it reads they cost 15%).
-template <bool kExplicit, bool kEager, bool kStream = false>
+template <bool kExplicit, bool kEager, bool kStream = false, bool kOff32 = false>
 __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
   State s;
   if (kStream)
-    s = State{__builtin_nontemporal_load(p.xi + i), __builtin_nontemporal_load(p.xdi + i),
-              __builtin_nontemporal_load(p.thi + i), __builtin_nontemporal_load(p.thdi + i)};
+    s = State{__builtin_nontemporal_load(elem<kOff32>(p.xi, i)),
+              __builtin_nontemporal_load(elem<kOff32>(p.xdi, i)),
+              __builtin_nontemporal_load(elem<kOff32>(p.thi, i)),
+              __builtin_nontemporal_load(elem<kOff32>(p.thdi, i))};
   else
-    s = State{p.xi[i], p.xdi[i], p.thi[i], p.thdi[i]};
-  if (kExplicit) a = uint32_t(p.actions[i] != 0);
-  fused_rest<kEager>(p, i, a, s, p.ep_len[i], kEager ? p.ep_index[i] : 0u);
+    s = State{*elem<kOff32>(p.xi, i), *elem<kOff32>(p.xdi, i), *elem<kOff32>(p.thi, i),
+              *elem<kOff32>(p.thdi, i)};
+  if (kExplicit) a = uint32_t(*elem<kOff32>(p.actions, i) != 0);
+  fused_rest<kEager, kOff32>(p, i, a, s, *elem<kOff32>(p.ep_len, i),
+                             kEager ? *elem<kOff32>(p.ep_index, i) : 0u);
 }
 
 // Concatenated-state level (the paper's baseline before its "no concat"
@@ -182,12 +218,14 @@ __global__ __launch_bounds__(kBlock) void k_concat_finish(StepParams p, const f3
   store_step(p, i, o, len, d, ret);
 }
 
-template <bool kExplicit, bool kEager, bool kStream = false>
+// kOff32 is launched only below kOff32MaxEnvs environments (kEager, below
+// kEagerMaxEnvs, always is).
+template <bool kExplicit, bool kEager, bool kStream, bool kOff32>
 __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
   // random actions: one block per wave, before any lane leaves
   const uint32_t a = kExplicit ? 0u : action_bit_wave(p.kact, p.env_base + i, p.t);
-  if (i < p.n) fused_one<kExplicit, kEager, kStream>(p, i, a);
+  if (i < p.n) fused_one<kExplicit, kEager, kStream, kOff32>(p, i, a);
 }
 
 // Horizontal fusion (the paper's horizontal fusion pass, Sec. "Fusion
@@ -204,11 +242,11 @@ __global__ __launch_bounds__(kBlock) void k_group_step(GroupParams g) {
   const StepParams &p = g.p[m];
   const uint32_t i = (blockIdx.x - g.first_block[m]) * kBlock + threadIdx.x;
   if (p.actions) {
-    if (i < p.n) fused_one<true, true>(p, i, 0u);
+    if (i < p.n) fused_one<true, true, false, false>(p, i, 0u);
   } else {
     // random actions: one block per wave, before any lane leaves
     const uint32_t a = action_bit_wave(p.kact, p.env_base + i, p.t);
-    if (i < p.n) fused_one<false, true>(p, i, a);
+    if (i < p.n) fused_one<false, true, false, false>(p, i, a);
   }
 }
 
@@ -248,17 +286,20 @@ __global__ __launch_bounds__(kBlock) void k_words(const GraphDesc *__restrict__ 
 
 // The latency-ordered fused step with the wave's actions from its word in
 // `row`.  Lanes past the batch load the last environment: no branch around
-// the loads, so nothing waits for them before the word is loaded.
+// the loads, so nothing waits for them before the word is loaded.  Built
+// into graphs only below kEagerMaxEnvs environments (32-bit offsets, as for
+// the kEager step).
 __global__ __launch_bounds__(kBlock) void k_fused_step_words(
     StepParams p, const unsigned long long *__restrict__ row) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
   const bool valid = i < p.n;
   const uint32_t ic = valid ? i : p.n - 1u;
-  const State s{p.xi[ic], p.xdi[ic], p.thi[ic], p.thdi[ic]};
-  const uint32_t len0 = p.ep_len[ic], k0 = p.ep_index[ic];
+  const State s{*elem<true>(p.xi, ic), *elem<true>(p.xdi, ic), *elem<true>(p.thi, ic),
+                *elem<true>(p.thdi, ic)};
+  const uint32_t len0 = *elem<true>(p.ep_len, ic), k0 = *elem<true>(p.ep_index, ic);
   const unsigned long long word = row[__builtin_amdgcn_readfirstlane(ic >> 6)];
   const uint32_t a = uint32_t(word >> (threadIdx.x & 63u)) & 1u;
-  if (valid) fused_rest<true>(p, i, a, s, len0, k0);
+  if (valid) fused_rest<true, true>(p, i, a, s, len0, k0);
 }
 
 __global__ __launch_bounds__(64) void k_graph_set(GraphDesc v, GraphDesc *d) {
@@ -300,6 +341,7 @@ std::vector<RolloutGraph> g_graphs;
 std::vector<RolloutKey> g_seen;  // kinds met once, oldest first
 
 hipError_t build_rollout_graph(const RolloutKey &k, hipGraphExec_t *out) {
+  if (k.base.n >= kEagerMaxEnvs) return hipErrorInvalidValue;
   hipGraph_t g = nullptr;
   hipError_t e = hipGraphCreate(&g, 0);
   if (e != hipSuccess) return e;
@@ -425,16 +467,21 @@ hipError_t launch_init(void *x, void *xd, void *th, void *thd, uint32_t *ep_inde
 
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
   const dim3 g = grid_for(p.n), b(kBlock);
-  const bool eager = p.n < kEagerMaxEnvs;
+  const bool eager = p.n < kEagerMaxEnvs, off32 = p.n < kOff32MaxEnvs;
   if (p.actions) {
-    if (eager) hipLaunchKernelGGL((k_fused_step<true, true>), g, b, 0, stream, p);
-    else hipLaunchKernelGGL((k_fused_step<true, false>), g, b, 0, stream, p);
+    if (eager) hipLaunchKernelGGL((k_fused_step<true, true, false, true>), g, b, 0, stream, p);
+    else if (off32)
+      hipLaunchKernelGGL((k_fused_step<true, false, false, true>), g, b, 0, stream, p);
+    else hipLaunchKernelGGL((k_fused_step<true, false, false, false>), g, b, 0, stream, p);
   } else if (eager) {
-    hipLaunchKernelGGL((k_fused_step<false, true>), g, b, 0, stream, p);
+    hipLaunchKernelGGL((k_fused_step<false, true, false, true>), g, b, 0, stream, p);
   } else if (p.xi != p.x) {  // state read from elsewhere than it is written
-    hipLaunchKernelGGL((k_fused_step<false, false, true>), g, b, 0, stream, p);
+    if (off32) hipLaunchKernelGGL((k_fused_step<false, false, true, true>), g, b, 0, stream, p);
+    else hipLaunchKernelGGL((k_fused_step<false, false, true, false>), g, b, 0, stream, p);
+  } else if (off32) {
+    hipLaunchKernelGGL((k_fused_step<false, false, false, true>), g, b, 0, stream, p);
   } else {
-    hipLaunchKernelGGL((k_fused_step<false, false>), g, b, 0, stream, p);
+    hipLaunchKernelGGL((k_fused_step<false, false, false, false>), g, b, 0, stream, p);
   }
   return hipGetLastError();
 }

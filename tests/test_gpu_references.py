@@ -47,6 +47,7 @@ def test_bad_arguments_are_refused(gpu):
     p = buf.data_ptr()
     st = torch.cuda.current_stream().cuda_stream
     assert r.cpref_touch(*([p] * 8), 0, st) == -1
+    assert r.cpref_touch(*([p] * 8), 1 << 30, st) == -1  # offsets past 32 bits
     assert r.cpref_touch(*([p] * 7), None, 64, st) == -1
     assert r.cpref_empty(0, st) == -1
     torch.cuda.synchronize()
