@@ -48,6 +48,9 @@ METRIC = "env-steps/sec on 1 MI355X; achieved HBM GB/s (or VALU %) vs peak"
 # steps) and is not counted.
 STEP_BYTES_WITH_OUTPUTS = 61
 STEP_BYTES_TRAJ_LARGE = 45
+# The whole-rollout kernel writing the same trajectory keeps the state in
+# registers: obs 16, reward 4, done 1 written per env-step, nothing read.
+STEP_BYTES_TRAJ_RESIDENT = 21
 # Algorithmic binary32 operations per environment-step of the dynamics
 # (sin, cos, 2 squares, 15 mul/add/sub/div in the accelerations, 8 in the
 # Euler update, 4 comparisons), each counted once.
@@ -97,10 +100,11 @@ def parse():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--only", choices=["headline", "resident_1024x200", "resident_1048576x1000",
                                        "resident_f64_1048576x1000", "resident_f16_1048576x1000",
-                                       "streaming_16777216x100", "policy_4194304x500",
+                                       "streaming_16777216x100", "resident_traj_16777216x100",
+                                       "policy_4194304x500",
                                        "policy_separate_4194304x500",
                                        "policy_two_streams_4194304x500", "horizontal_16x4096",
-                                       "copy",
+                                       "copy", "fill",
                                        "valu_reference", "graph_floor"],
                     help="run one workload only (for counter collection); prints its JSON")
     return ap.parse_args()
@@ -193,6 +197,18 @@ def bench_copy():
     wall, ev = timed(lambda: torch.mul(src, 1.0, out=dst), reps=5)
     return {"bytes_read": 1 << 30, "bytes_written": 1 << 30, "ms": ev / 5,
             "GB_per_s": 2 * (1 << 30) / (ev / 5 * 1e-3) / 1e9}
+
+
+def bench_fill():
+    """A plain 4 GiB fill (writes only): the write-bandwidth reference for
+    kernels that only write HBM, such as the whole-rollout kernel writing a
+    trajectory."""
+    import torch
+
+    dst = torch.empty(1 << 30, device="cuda")
+    dst.fill_(1.0)
+    wall, ev = timed(lambda: dst.fill_(2.0), reps=5)
+    return {"bytes_written": 1 << 32, "ms": ev / 5, "GB_per_s": (1 << 32) / (ev / 5 * 1e-3) / 1e9}
 
 
 VALU_REFERENCE_FORMS = ("fma_f32_vgpr", "fma_f32_sgpr_operand", "rotate_u32", "rcp_f32", "fma_f64",
@@ -300,6 +316,8 @@ def bench_configs(cp, only=None):
         res["resident_f16_1048576x1000"] = _resident_large(cp, "f16")
     if want("streaming_16777216x100"):
         res["streaming_16777216x100"] = _streaming(cp)
+    if want("resident_traj_16777216x100"):
+        res["resident_traj_16777216x100"] = _resident_traj(cp)
     if want("policy_4194304x500"):
         res["policy_4194304x500"] = _policy(cp)
     if want("policy_separate_4194304x500"):
@@ -419,6 +437,28 @@ def _streaming(cp):
            "kernel_mean_us": mean_ms * 1e3,
            "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                         "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": STEP_BYTES_TRAJ_LARGE}}
+    del s, tr
+    torch.cuda.empty_cache()
+    return out
+
+
+def _resident_traj(cp):
+    import torch
+
+    # the same 16,777,216 x 100 trajectory from the whole-rollout kernel
+    # (state in registers; the trajectory is the only HBM traffic)
+    n, T = 1 << 24, 100
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    cp.cp_init(s, 0)
+    tr = cp.Trajectory(n, T, stats=False, totals=False)
+    cp.cp_rollout(s, T, 0, tr)
+    wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=3)
+    ms = ev / 3
+    gbs = STEP_BYTES_TRAJ_RESIDENT * n * T / (ms * 1e-3) / 1e9
+    out = {"env_steps_per_s": n * T / (ms * 1e-3), "ms": ms,
+           "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                        "frac": gbs / HBM_PEAK_GBS,
+                        "bytes_per_env_step": STEP_BYTES_TRAJ_RESIDENT}}
     del s, tr
     torch.cuda.empty_cache()
     return out
@@ -628,7 +668,7 @@ def main():
         print(json.dumps({"only": "headline", **head["fused"]}))
         return
     if args.only:
-        refs = {"copy": bench_copy, "valu_reference": bench_valu_reference,
+        refs = {"copy": bench_copy, "fill": bench_fill, "valu_reference": bench_valu_reference,
                 "graph_floor": bench_graph_floor}
         res = refs[args.only]() if args.only in refs else bench_configs(cp, args.only)[args.only]
         print(json.dumps({"only": args.only, **res}))
@@ -672,7 +712,8 @@ def main():
     if not args.quick:
         line["configs"] = bench_configs(cp)
         line["unroll"] = bench_unroll(cp)
-        line["references"] = {"copy": bench_copy(), "valu": bench_valu_reference(),
+        line["references"] = {"copy": bench_copy(), "fill": bench_fill(),
+                              "valu": bench_valu_reference(),
                               "graph_floor": bench_graph_floor(kern_us)}
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline()

@@ -227,6 +227,33 @@ __device__ __forceinline__ bool terminated(State s) {
   return s.x < -kXLimit || s.x > kXLimit || s.th < -kThetaLimit || s.th > kThetaLimit;
 }
 
+// ---------------------------------------------------------------- addressing
+// Accesses through pointers that the compiler cannot place in global memory
+// by itself (pointers loaded from memory rather than passed as kernel
+// arguments) are typed as global, so that they compile to global rather
+// than flat instructions.
+template <class T>
+using global_ptr = __attribute__((address_space(1))) T *;
+
+// Element i of a global array.  kOff32: the caller guarantees that the byte
+// offset i * sizeof(T) fits in 32 bits, and the access takes the array's
+// scalar base plus a 32-bit vector offset instead of a 64-bit vector address
+// computed per array (in the one-step-per-launch step, where one wave per
+// SIMD runs its instructions back to back, that 64-bit arithmetic cost 12%
+// of the step).  The offset passes an empty volatile asm at each use so that
+// the compiler widens it next to the access, where the scalar-base form is
+// selected, rather than once for all accesses and then adds it to each base
+// in 64-bit vector arithmetic.
+template <bool kOff32, class T>
+__device__ __forceinline__ global_ptr<T> elem(T *base, uint32_t i) {
+  if (kOff32) {
+    uint32_t off = i * uint32_t(sizeof(T));
+    asm volatile("" : "+v"(off));
+    return (global_ptr<T>)((__attribute__((address_space(1))) char *)base + off);
+  }
+  return (global_ptr<T>)base + i;
+}
+
 // ---------------------------------------------------------------- wave helpers
 __device__ __forceinline__ uint32_t wave_sum_u32(uint32_t v) {
 #pragma unroll

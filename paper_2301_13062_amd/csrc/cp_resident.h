@@ -110,6 +110,26 @@ struct HashPolicy {
   }
 };
 
+// Stores of the j-th step of a trajectory: obs [T][4][n] in the state's
+// type, reward [T][n] f32, done [T][n] u8.  Each plane's base for the step
+// is wave-uniform (scalar arithmetic); kOff32 (every byte offset within a
+// plane below 2^32) takes the scalar-base form with the lane's fixed 32-bit
+// offset, otherwise 64-bit vector addresses.
+template <bool kOff32, class T, class S>
+__device__ __forceinline__ void store_traj(const RolloutParams &p, T *pobs, uint32_t j, uint32_t i,
+                                           const S &s, bool d) {
+  const size_t plane = size_t(j) * p.n;
+  if (p.obs) {
+    T *const ob = pobs + 4u * plane;
+    __builtin_nontemporal_store(s.x, elem<kOff32>(ob, i));
+    __builtin_nontemporal_store(s.xd, elem<kOff32>(ob + p.n, i));
+    __builtin_nontemporal_store(s.th, elem<kOff32>(ob + 2u * size_t(p.n), i));
+    __builtin_nontemporal_store(s.thd, elem<kOff32>(ob + 3u * size_t(p.n), i));
+  }
+  if (p.reward) __builtin_nontemporal_store(1.0f, elem<kOff32>(p.reward + plane, i));
+  if (p.done) __builtin_nontemporal_store(uint8_t(d), elem<kOff32>(p.done + plane, i));
+}
+
 // The loop.  `policy(j, t, s)` returns the action of step t (j-th of this
 // rollout) for the lane's pre-step state s; it is called by every lane of
 // the wave at every step (policies may use cross-lane operations).  P is
@@ -125,6 +145,9 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
   T *const pthd = reinterpret_cast<T *>(p.thd);
   T *const pobs = reinterpret_cast<T *>(p.obs);
   const uint32_t i = blockIdx.x * kResidentBlock + threadIdx.x;
+  // every byte offset within a trajectory plane (at most max(sizeof(T), 4)
+  // bytes per environment) below 2^32
+  const bool off32 = uint64_t(p.n) * (sizeof(T) > 4 ? sizeof(T) : 4) <= (uint64_t(1) << 32);
   const bool valid = i < p.n;
   const uint32_t env = p.env_base + i;
   // Lanes past the end run the loop on a dummy state (the wave stays
@@ -155,16 +178,8 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
     have = have && !d;
     s = o;
     if (kTraj && valid) {
-      const size_t base = size_t(j) * p.n + i;
-      if (p.obs) {
-        const size_t ob = size_t(j) * 4u * p.n + i;
-        __builtin_nontemporal_store(s.x, pobs + ob);
-        __builtin_nontemporal_store(s.xd, pobs + ob + p.n);
-        __builtin_nontemporal_store(s.th, pobs + ob + 2u * p.n);
-        __builtin_nontemporal_store(s.thd, pobs + ob + 3u * p.n);
-      }
-      if (p.reward) __builtin_nontemporal_store(1.0f, p.reward + base);
-      if (p.done) __builtin_nontemporal_store(uint8_t(d), p.done + base);
+      if (off32) store_traj<true>(p, pobs, j, i, s, d);
+      else store_traj<false>(p, pobs, j, i, s, d);
     }
     wave_done += __popcll(__ballot(d));
   };

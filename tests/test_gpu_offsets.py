@@ -121,3 +121,55 @@ def test_fused_rollout_with_trajectory_at_the_offset_limit(gpu, n):
     assert np.array_equal(k[match], o.ep_index[match]) and np.array_equal(ln[match], o.ep_len[match])
     del s, tr
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("n", SIZES, ids=IDS)
+def test_resident_rollout_with_trajectory_at_the_offset_limit(gpu, n):
+    # the whole-rollout kernel's trajectory stores: each step's planes from
+    # scalar bases with the lane's fixed 32-bit offset below the limit
+    seed, act_seed, T = 24, 25, 3
+    ids = sample(n, 3)
+    idx = torch.from_numpy(ids).cuda()
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    cp.cp_init(s, seed)
+    tr = cp.Trajectory(n, T, stats=False, totals=False)
+    cp.cp_rollout(s, T, act_seed, tr)
+    torch.cuda.synchronize()
+    g_obs = cols(tr.obs, idx)
+    g_done = cols(tr.done, idx)
+    assert bool((tr.reward == 1.0).all())
+    assert np.array_equal(g_obs[-1], state_at(s, idx))
+    o = O.OracleState(len(ids), ids.astype(np.uint32))
+    O.init(o, seed)
+    out = O.rollout(o, T, act_seed=act_seed, traj=True)
+    match = (g_done == out["done"]).all(axis=0)
+    assert match.mean() >= ROLL_MATCH
+    err = np.abs(g_obs[:, :, match].astype(np.float64) - out["obs"][:, :, match])
+    assert err.max() <= ROLL_ABS
+    del s, tr
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("n", [(1 << 29) - 1, 1 << 29], ids=["below_2^29", "at_2^29"])
+def test_resident_binary64_trajectory_at_the_offset_limit(gpu, n):
+    # binary64 obs planes hold 8 bytes per environment: the limit is 2^29
+    seed, act_seed, T = 26, 27, 2
+    ids = sample(n, 4)
+    idx = torch.from_numpy(ids).cuda()
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, precision=cp.CP_PREC_F64)
+    cp.cp_init(s, seed)
+    tr = cp.Trajectory(n, T, dtype=torch.float64, stats=False, totals=False)
+    cp.cp_rollout(s, T, act_seed, tr)
+    torch.cuda.synchronize()
+    g_obs = cols(tr.obs, idx)
+    g_done = cols(tr.done, idx)
+    assert np.array_equal(g_obs[-1], state_at(s, idx))
+    o = O.OracleStateP(len(ids), O.F64, ids.astype(np.uint32))
+    O.init_prec(o, seed)
+    out = O.rollout_prec(o, T, act_seed=act_seed, traj=True)
+    match = (g_done == out["done"]).all(axis=0)
+    assert match.mean() >= ROLL_MATCH
+    err = np.abs(g_obs[:, :, match] - out["obs"][:, :, match])
+    assert err.max() <= 1e-9
+    del s, tr
+    torch.cuda.empty_cache()
