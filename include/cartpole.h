@@ -19,7 +19,10 @@
  *
  * Conventions shared by every entry point:
  *  - Every pointer inside cp_states / cp_traj is a DEVICE pointer owned by the
- *    caller; the library never allocates, frees or retains memory.
+ *    caller; the library never allocates, frees or retains the caller's
+ *    memory and calls no allocator itself.  The one thing it keeps is the
+ *    cache of instantiated HIP graphs of cp_rollout (below): runtime objects,
+ *    whose kernel-argument storage the HIP runtime provides.
  *  - Calls are asynchronous on s->stream (a hipStream_t; NULL = the null
  *    stream).  Results are visible after the caller synchronises it.
  *  - Return value: CP_OK (0) or a negative CP_ERR_* code; cp_last_error()

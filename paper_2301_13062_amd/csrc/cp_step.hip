@@ -92,9 +92,10 @@ __device__ __forceinline__ void store_step(const StepParams &p, uint32_t i, cons
 // The fused step of one environment after its loads: s, its running
 // episode length and (kEager) its episode index k0.  kEager (small batches,
 // where a step is latency-bound): the episode index was loaded with the
-// state and the next start state is drawn while the dynamics run, instead of
-// a second memory round trip and the draw after the termination test; the
-// episode index is still written only on termination.  kOff32: as for
+// state and every lane draws the next start state besides running the
+// dynamics, instead of a second memory round trip and the draw after the
+// termination test; the episode index is still written only on
+// termination.  kOff32: as for
 // elem(), for every array the step touches.
 template <bool kEager, bool kOff32>
 __device__ __forceinline__ void fused_rest(const StepParams &p, uint32_t i, uint32_t a,
