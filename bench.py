@@ -70,7 +70,7 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 # flags: the counters below stand for it only while these are unchanged.
 COUNTER_SOURCES = ["paper_2301_13062_amd/csrc/cp_step.hip", "paper_2301_13062_amd/csrc/cp_device.h",
                    "paper_2301_13062_amd/csrc/cp_launch.h"]
-COUNTERS = {"sources_sha256_16": "a43b34df8e7c480b",
+COUNTERS = {"sources_sha256_16": "cbdc6a566c9f748a",
             "fused_step_65536": {"fetch_kib": 812.0, "write_kib": 2703.0},
             "read_factor": 1.99995, "write_factor": 1.0}
 
