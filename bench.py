@@ -708,6 +708,12 @@ def main():
         "fused_direct": {"env_steps_per_s": head["fused_direct"]["env_steps_per_s"],
                          "us_per_step": head["fused_direct"]["us_per_step"]},
         "graph_speedup": fused["env_steps_per_s"] / head["fused_direct"]["env_steps_per_s"],
+        # the same ratios with every level launched from the host step by step
+        # (the unfused and concat levels are not graph-replayed)
+        "fusion_speedup_host_launched": head["fused_direct"]["env_steps_per_s"]
+        / head["unfused"]["env_steps_per_s"],
+        "no_concat_speedup_host_launched": head["fused_direct"]["env_steps_per_s"]
+        / head["concat"]["env_steps_per_s"],
     }
     if not args.quick:
         line["configs"] = bench_configs(cp)
