@@ -252,6 +252,9 @@ def test_rollout_16m_x_100_streaming_sampled(gpu):
     match = assert_rollout_match(g_done, out["done"], g, o.state())
     err = np.abs(g_obs[:, :, match].astype(np.float64) - out["obs"][:, :, match])
     assert err.max() <= ROLL_ABS
+    gk = u32(s.ep_index.index_select(0, idx))
+    gl = u32(s.ep_len.index_select(0, idx))
+    assert np.array_equal(gk[match], o.ep_index[match]) and np.array_equal(gl[match], o.ep_len[match])
     del tr
     torch.cuda.empty_cache()
 
@@ -268,6 +271,41 @@ def test_large_batch_fused_trajectory_equals_resident(gpu):
     for f in ("obs", "reward", "done", "totals"):
         assert torch.equal(getattr(ft, f), getattr(rt, f)), f
     assert torch.equal(ft.obs[-1], fs.state())
+
+
+@pytest.mark.parametrize("case", ["done_planes", "with_stats", "no_done", "one_step", "long_episodes"])
+def test_large_batch_episode_lengths_equal_resident(gpu, case):
+    # From 2^21 environments the fused rollout reads each step's state from
+    # the previous obs plane; with or without done flags and per-environment
+    # statistics, the episode counters, the totals and the trajectory equal
+    # the resident kernel's bit for bit -- also for one step, and for
+    # caller-loaded lengths near the top of the u32 range (some of which
+    # wrap).
+    n = (1 << 21) + 37
+    T = 1 if case == "one_step" else 20
+    kw = dict(stats=case == "with_stats", done=case != "no_done")
+
+    def go(variant):
+        s = cp.CartPoleStates(n, variant=variant)
+        cp.cp_init(s, 4)
+        if case == "long_episodes":
+            g = torch.Generator(device="cuda").manual_seed(1)
+            s.ep_len.copy_(torch.randint(-(1 << 31), 1 << 31, (n,), dtype=torch.int32,
+                                         device="cuda", generator=g))
+        tr = cp.Trajectory(n, T, **kw)
+        cp.cp_rollout(s, T, 9, tr)
+        torch.cuda.synchronize()
+        return s, tr
+
+    fs, ft = go(cp.CP_FUSED)
+    rs, rt = go(cp.CP_RESIDENT)
+    assert torch.equal(fs.state(), rs.state())
+    assert torch.equal(fs.ep_index, rs.ep_index) and torch.equal(fs.ep_len, rs.ep_len)
+    for f in ("obs", "reward", "done", "done_count", "total_reward", "ret_sum", "totals"):
+        a, b = getattr(ft, f), getattr(rt, f)
+        assert (a is None) == (b is None), f
+        if a is not None:
+            assert torch.equal(a, b), f
 
 
 @pytest.mark.parametrize("k", [1, 3, 7, 64])
