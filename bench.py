@@ -4,22 +4,36 @@ Headline (the JSON line's `value`): 65,536 environments advanced one step
 per kernel launch by the fused step kernel, random actions, each step
 writing obs / reward / done -- the configuration on which the paper's
 fusion comparison is made (unfused per-op chain vs one fused kernel).  A
-"step" of this benchmark is one such launch over the whole batch.
+"step" of this benchmark is one such launch over the whole batch, replayed
+from the library's HIP graph.
 
 Also measured in the same run (extra keys of the same JSON line):
-  unfused   the same workload through the one-op-per-kernel chain;
-  concat    the same workload split into two kernels at a concatenation of
-            the updated state (the paper's baseline before "no concat");
-  configs   1,024 x 200 and 1,048,576 x 1,000 register-resident rollouts,
-            16,777,216 x 100 streaming fused steps with full trajectory,
-            4,194,304 x 500 with the MLP policy on the matrix cores;
-  roofline  HBM roofline of the fused step kernel: algorithmic bytes per
-            launch over the mean launch duration (HIP events around the
-            timed region of back-to-back launches, divided by the launches);
-  cpu_baseline  the CPU oracle on the host cores (one thread), and a
-            small-batch sweep against the resident kernel (crossover).
+  roofline      HBM roofline of the headline kernel: algorithmic bytes per
+                launch over the mean launch duration (HIP events around the
+                timed region, divided by the launches), and the HBM traffic
+                from stored counter readings while the kernel sources match;
+  unfused, concat, fused_direct
+                the same workload through the one-op-per-kernel chain, split
+                at a concatenation of the updated state (the paper's baseline
+                before "no concat"), and the fused kernel launched from the
+                host step by step; speedups against each, also like for like
+                (every level host-launched);
+  configs       register-resident rollouts (1,024 x 200; 1,048,576 x 1,000 in
+                binary32, binary64 and binary16), 16,777,216 x 100 with the
+                full trajectory (streaming fused steps, and the resident
+                kernel writing the same trajectory), 4,194,304 x 500 with the
+                MLP policy (fused; and as separate kernels on one or two
+                streams), 16 batches x 4,096 stepped by one grouped launch;
+  unroll        the resident kernel at k steps per launch (k = 1 ... 1,000);
+  references    a plain copy and fill (bandwidth), issue rates per vector
+                instruction class, and the per-node floors of graph replay
+                (reference kernels of libcpref.so);
+  cpu_baseline  the CPU oracle on the host cores (one thread, and all of
+                them), a small-batch sweep against the resident kernel
+                (crossover) and the oracle's rate per configuration.
 
-Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick]
+Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick] [--no-cpu]
+                       [--only NAME]   (one workload or reference, its JSON only)
 """
 import argparse
 import json
