@@ -2,7 +2,8 @@
 repeats an earlier call's arrays, outputs and length) against the same
 rollouts launched step by step from the host: bit for bit, replay after
 replay, with the program's own work and synchronisations between calls,
-interleaved handles, and under a caller's own stream capture."""
+interleaved handles, two host threads at once, and under a caller's own
+stream capture."""
 import pytest
 import torch
 
@@ -126,3 +127,54 @@ def test_more_kinds_than_the_graph_cache_holds(gpu):
             cp.cp_rollout(b, T, T, tb)
             torch.cuda.synchronize()
             assert_same(a, b, ta, tb)
+
+
+def test_two_threads_replay_concurrently(gpu):
+    # Two host threads each drive their own handle on their own stream; the
+    # library's graph cache (shared, behind a lock) serves both at once, and
+    # every call equals the same rollout launched step by step on one thread.
+    import threading
+
+    specs = [(4096, 11, 0), (3001, 12, 70)]
+    reps, T = 6, 64
+    refs = []
+    for n, seed, base in specs:
+        b = cp.CartPoleStates(n, variant=cp.CP_FUSED, env_base=base, graphs=False)
+        cp.cp_init(b, seed)
+        tb = cp.Trajectory(n, T)
+        outs = []
+        for _ in range(reps):
+            cp.cp_rollout(b, T, seed + 1, tb)
+            torch.cuda.synchronize()
+            outs.append((b.state().clone(), tb.obs.clone(), tb.done.clone(), tb.totals.clone()))
+        refs.append(outs)
+    results, errors = [None] * len(specs), []
+
+    def worker(k):
+        try:
+            n, seed, base = specs[k]
+            st = torch.cuda.Stream()
+            with torch.cuda.stream(st):
+                a = cp.CartPoleStates(n, variant=cp.CP_FUSED, env_base=base, graphs=True)
+                cp.cp_init(a, seed)
+                ta = cp.Trajectory(n, T)
+                outs = []
+                for _ in range(reps):
+                    cp.cp_rollout(a, T, seed + 1, ta)
+                    outs.append((a.state().clone(), ta.obs.clone(), ta.done.clone(),
+                                 ta.totals.clone()))
+            st.synchronize()
+            results[k] = outs
+        except Exception as e:  # reported by the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(len(specs))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=120)
+    assert not errors, errors
+    assert all(r is not None for r in results)
+    for outs, ref in zip(results, refs):
+        for got, want in zip(outs, ref):
+            assert all(torch.equal(x, y) for x, y in zip(got, want))
