@@ -74,35 +74,75 @@ POLICY_FLOPS = 2 * (4 * 64 + 64 * 64 + 64 * 2)
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 
 
-# HBM traffic of one launch of the headline kernel (fused step, 65,536
-# environments) from two rocprofv3 counter passes (FETCH_SIZE, WRITE_SIZE,
-# KiB per dispatch), scaled by the same counters' reading for a plain 1 GiB
-# copy (read factor 1.99995, write factor 1.0).  Valid only for the kernel
-# sources they were taken on; any change to them makes the figure null
-# until the counters are taken again.
-# The files the headline kernel's code is compiled from, and the compiler
-# flags: the counters below stand for it only while these are unchanged.
-COUNTER_SOURCES = ["paper_2301_13062_amd/csrc/cp_step.hip", "paper_2301_13062_amd/csrc/cp_device.h",
-                   "paper_2301_13062_amd/csrc/cp_launch.h"]
-COUNTERS = {"sources_sha256_16": "cbdc6a566c9f748a",
-            "fused_step_65536": {"fetch_kib": 812.0, "write_kib": 2703.0},
-            "read_factor": 1.99995, "write_factor": 1.0}
+# Counter readings (rocprofv3 --pmc passes, summarised with their commands
+# in profiles/) of three kernels.  Each holds only for the sources its
+# kernel's code is compiled from and the compiler flags it was taken with
+# (a sha256 prefix over their contents and the flags); a stale entry reads
+# as null until the counters are taken again.
+_CSRC = "paper_2301_13062_amd/csrc/"
+COUNTERS = {
+    # HBM traffic of one headline launch (fused step, 65,536 environments):
+    # FETCH_SIZE and WRITE_SIZE, KiB per dispatch
+    "fused_step_65536": {
+        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_device.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "cbdc6a566c9f748a", "fetch_kib": 812.0, "write_kib": 2703.0},
+    # the resident rollout, 1,048,576 x 1,000: SQ_INSTS_VALU per wave-step
+    "resident_1048576x1000": {
+        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
+                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "8fdcd8aed35b7edf", "valu_per_wave_step": 71.6},
+    # the MLP-policy rollout, 4,194,304 x 500: SQ_INSTS_VALU per wave-step and
+    # the matrix cores' busy share of SIMD cycles (SQ_VALU_MFMA_BUSY_CYCLES)
+    "policy_4194304x500": {
+        "sources": [_CSRC + "cp_policy.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
+                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "a6e1296e5e96d224", "valu_per_wave_step": 1937.2, "mfma_busy": 0.218},
+}
+# The same counters' reading for a plain 1 GiB copy (1 GiB read, 1 GiB
+# written): bytes per KiB counted.
+READ_FACTOR, WRITE_FACTOR = 1.99995, 1.0
+# Vector-instruction issue: a CU issues at most two wave64 VALU instructions
+# per cycle (4 SIMDs, one every 2 cycles each), at most 2.4 GHz.
+ISSUE_PEAK_PER_CU_CYCLE, CLOCK_PEAK_HZ, CUS = 2.0, 2.4e9, 256
 
 
-def measured_traffic_bytes(key):
+def sources_sha(files):
     import hashlib
 
     from paper_2301_13062_amd import build as B
 
     h = hashlib.sha256()
-    for f in COUNTER_SOURCES:
+    for f in files:
         with open(os.path.join(ROOT, f), "rb") as fh:
             h.update(fh.read())
     h.update(" ".join(B.FLAGS).encode())
-    if h.hexdigest()[:16] != COUNTERS["sources_sha256_16"]:
-        return None
+    return h.hexdigest()[:16]
+
+
+def stored_counters(key):
     c = COUNTERS[key]
-    return 1024 * (c["fetch_kib"] * COUNTERS["read_factor"] + c["write_kib"] * COUNTERS["write_factor"])
+    return c if sources_sha(c["sources"]) == c["sha256_16"] else None
+
+
+def measured_traffic_bytes(key):
+    c = stored_counters(key)
+    if c is None:
+        return None
+    return 1024 * (c["fetch_kib"] * READ_FACTOR + c["write_kib"] * WRITE_FACTOR)
+
+
+def valu_issue(key, env_steps_per_s):
+    """VALU issue of a resident kernel: its counter-measured instructions per
+    wave-step at the measured env-steps/s, per CU per cycle at the peak
+    clock, against the issue peak (the clock under load is lower, so the
+    share of the cycles actually run is higher still)."""
+    c = stored_counters(key)
+    if c is None:
+        return None
+    per_cycle = c["valu_per_wave_step"] * env_steps_per_s / 64 / CUS / CLOCK_PEAK_HZ
+    return {"valu_per_wave_step": c["valu_per_wave_step"], "per_cu_per_cycle": per_cycle,
+            "peak_per_cu_per_cycle": ISSUE_PEAK_PER_CU_CYCLE,
+            "frac": per_cycle / ISSUE_PEAK_PER_CU_CYCLE, "clock_ghz": CLOCK_PEAK_HZ / 1e9}
 
 
 def parse():
@@ -428,11 +468,14 @@ def _resident_large(cp, precision="f32"):
     mean_ms = ev / 5
     eps = n * T / (mean_ms * 1e-3)
     peak = VALU_PEAK_TOPS / 2 if precision == "f64" else VALU_PEAK_TOPS
-    return {"env_steps_per_s": eps, "ms": mean_ms,
-            "roofline": {"bound": "alu", "achieved": eps * STEP_FLOPS / 1e12,
-                         "peak": peak, "unit": "TOP/s",
-                         "frac": eps * STEP_FLOPS / 1e12 / peak,
-                         "ops_per_env_step": STEP_FLOPS}}
+    out = {"env_steps_per_s": eps, "ms": mean_ms,
+           "roofline": {"bound": "alu", "achieved": eps * STEP_FLOPS / 1e12,
+                        "peak": peak, "unit": "TOP/s",
+                        "frac": eps * STEP_FLOPS / 1e12 / peak,
+                        "ops_per_env_step": STEP_FLOPS}}
+    if precision == "f32":
+        out["valu_issue"] = valu_issue("resident_1048576x1000", eps)
+    return out
 
 
 def _streaming(cp):
@@ -495,10 +538,13 @@ def _policy(cp):
     ms = ev / 3
     eps = n * T / (ms * 1e-3)
     tflops = eps * POLICY_FLOPS / 1e12
+    c = stored_counters("policy_4194304x500")
     return {"env_steps_per_s": eps, "ms": ms,
             "roofline": {"bound": "mfma", "achieved": tflops, "peak": BF16_MFMA_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": tflops / BF16_MFMA_PEAK_TFLOPS,
-                         "flops_per_env_step": POLICY_FLOPS}}
+                         "flops_per_env_step": POLICY_FLOPS},
+            "valu_issue": valu_issue("policy_4194304x500", eps),
+            "mfma_busy_frac": c["mfma_busy"] if c else None}
 
 
 def _policy_separate(cp, streams):
