@@ -91,6 +91,15 @@ COUNTERS = {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
                     _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
         "sha256_16": "8fdcd8aed35b7edf", "valu_per_wave_step": 71.6},
+    # the same rollout stepped in binary64 and in binary16
+    "resident_f64_1048576x1000": {
+        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
+                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "8fdcd8aed35b7edf", "valu_per_wave_step": 97.8},
+    "resident_f16_1048576x1000": {
+        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
+                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "8fdcd8aed35b7edf", "valu_per_wave_step": 105.9},
     # the MLP-policy rollout, 4,194,304 x 500: SQ_INSTS_VALU per wave-step and
     # the matrix cores' busy share of SIMD cycles (SQ_VALU_MFMA_BUSY_CYCLES)
     "policy_4194304x500": {
@@ -473,8 +482,8 @@ def _resident_large(cp, precision="f32"):
                         "peak": peak, "unit": "TOP/s",
                         "frac": eps * STEP_FLOPS / 1e12 / peak,
                         "ops_per_env_step": STEP_FLOPS}}
-    if precision == "f32":
-        out["valu_issue"] = valu_issue("resident_1048576x1000", eps)
+    out["valu_issue"] = valu_issue("resident_1048576x1000" if precision == "f32"
+                                   else f"resident_{precision}_1048576x1000", eps)
     return out
 
 
