@@ -64,6 +64,15 @@ MUTANTS = {
                            "orc_reset_state(reset_seed, env, t, next);"),
     # MLP policy
     "mlp_transpose": ("w[i * n_out + j]", "w[j * n_in + i]"),
+    "mlp_no_bf16_input": ("in[i] = orc_f32_from_bf16(orc_bf16_from_f32(obs[i]));",
+                          "in[i] = obs[i];"),
+    "mlp_no_bf16_first_hidden": (
+        "h1[j] = orc_f32_from_bf16(orc_bf16_from_f32((float)tanh((double)z1[j])));",
+        "h1[j] = (float)tanh((double)z1[j]);"),
+    "mlp_tie_picks_one": ("return z3[1] > z3[0] ? 1 : 0;", "return z3[1] >= z3[0] ? 1 : 0;"),
+    "mlp_binary32_sums": ("        double acc = 0.0;", "        float acc = 0.0f;"),
+    "bf16_truncates": ("u += 0x7FFFu + lsb;", "u += 0u * lsb;"),
+    "bf16_ties_away": ("u += 0x7FFFu + lsb;", "u += 0x8000u + 0u * lsb;"),
     "mlp_no_bf16_hidden": (
         "h2[j] = orc_f32_from_bf16(orc_bf16_from_f32((float)tanh((double)z2[j])));",
         "h2[j] = (float)tanh((double)z2[j]);"),

@@ -442,6 +442,29 @@ def test_mlp_hand_computed_path():
     assert O.mlp_action(wx, [0.5, 0.0, -0.03, 0.0])[0] == 1
 
 
+def test_mlp_layer_sums_are_rounded_once():
+    # Each pre-activation is the exact sum of its products, rounded once to
+    # binary32 (the reading of the dense layers); a running binary32 sum
+    # gives another value here.  x = 1 and W1[0][:] = 10 drive every hidden
+    # unit to tanh(10) and tanh(64), both 1 in binary32, so h2 is all ones;
+    # then logit 0 = 1 + 63 * 2^-24 exactly, which rounds (a tie, to even) to
+    # 1 + 2^-18, while a running binary32 sum never leaves 1.  Logit 1 =
+    # 1 + 2^-19 sits between the two, so the action tells them apart too.
+    from fractions import Fraction
+
+    w1 = [((0, j), 10.0) for j in range(64)]
+    w2 = [((i, j), 1.0) for i in range(64) for j in range(64)]
+    w3 = [((0, 0), 1.0)] + [((i, 0), 2.0 ** -24) for i in range(1, 64)]
+    w3 += [((0, 1), 1.0), ((1, 1), 2.0 ** -19)]
+    w = _one_hot_weights(w1=w1, w2=w2, w3=w3)
+    a, logits = O.mlp_action(w, [1.0, 0.0, 0.0, 0.0])
+    exact0 = Fraction(1) + 63 * Fraction(1, 2 ** 24)
+    assert float(exact0) != 1.0 + 2.0 ** -18  # the exact sum is a binary32 tie
+    assert logits[0] == np.float32(1.0 + 2.0 ** -18)
+    assert logits[1] == np.float32(1.0 + 2.0 ** -19)
+    assert a == 0
+
+
 def test_mlp_matches_float64_matmul():
     # Library-routine cross-check: layer by layer with numpy float64 matmul on
     # the same bf16-rounded operands (rounding to f32 at the same points).
