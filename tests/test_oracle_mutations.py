@@ -38,6 +38,20 @@ MUTANTS = {
         "out[1] = xd + tau * xacc;\n    out[0] = x + tau * out[1];\n"
         "    out[3] = thd + tau * thacc;\n    out[2] = th + tau * out[3];\n}\n\n/* The same"),
     # binary32 termination
+    "obs_before_reset": ("                orc_reset_state(reset_seed, env, k, next);\n            }\n            memcpy(s, next, sizeof s);\n\n            if (obs)\n                for (int j = 0; j < 4; ++j) obs[(step * 4 + j) * m + i] = s[j];",
+                         "                orc_reset_state(reset_seed, env, k, s);\n            }\n            if (!d) memcpy(s, next, sizeof s);\n\n            if (obs)\n                for (int j = 0; j < 4; ++j) obs[(step * 4 + j) * m + i] = next[j];"),
+    "no_reward_on_termination": ("int d = orc_terminated_f32(next);\n            float r = 1.0f;",
+                                 "int d = orc_terminated_f32(next);\n            float r = d ? 0.0f : 1.0f;"),
+    "length_kept_after_termination": ("                len = 0u;\n                k += 1u;\n                orc_reset_state(",
+                                      "                k += 1u;\n                orc_reset_state("),
+    "return_excludes_terminal_step": (
+        "                returns += len;\n                n_done += 1u;\n                len = 0u;\n"
+        "                k += 1u;\n                orc_reset_state(",
+        "                returns += len - 1u;\n                n_done += 1u;\n                len = 0u;\n"
+        "                k += 1u;\n                orc_reset_state("),
+    "reset_keyed_by_old_episode": ("                k += 1u;\n                orc_reset_state(reset_seed, env, k, next);",
+                                   "                orc_reset_state(reset_seed, env, k, next);\n                k += 1u;"),
+    "terminated_on_old_state": ("            int d = orc_terminated_f32(next);", "            int d = orc_terminated_f32(s);"),
     "threshold_decimal": ("(float)(12.0 * 2.0 * 3.14159265358979323846 / 360.0)", "0.20944f"),
     "ge_not_gt": ("const float x_limit = 2.4f;", "const float x_limit = 2.4f * 0.9999999f;"),
     # generator, actions, start states
