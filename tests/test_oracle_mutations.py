@@ -93,6 +93,18 @@ MUTANTS = {
     # binary64
     "f64_missing_c": ("const double xacc = temp - pml * thacc * c / m;",
                       "const double xacc = temp - pml * thacc / m;"),
+    "f64_gravity_sign": ("const double thacc = (g * sn - c * temp) / (l * (four3 - mp * c2 / m));",
+                         "const double thacc = (-g * sn - c * temp) / (l * (four3 - mp * c2 / m));"),
+    "f64_semi_implicit_euler": (
+        "const double xacc = temp - pml * thacc * c / m;\n\n    out[0] = x + tau * xd;\n"
+        "    out[1] = xd + tau * xacc;",
+        "const double xacc = temp - pml * thacc * c / m;\n\n    out[1] = xd + tau * xacc;\n"
+        "    out[0] = x + tau * out[1];"),
+    "f16_gravity_sign": ("const double thacc = h(h(h(g * sn) - h(c * temp))",
+                         "const double thacc = h(h(h(-g * sn) - h(c * temp))"),
+    "f16_semi_implicit_euler": ("    out[2] = h(th + h(tau * thd));\n    out[3] = h(thd + h(tau * thacc));",
+                                "    out[3] = h(thd + h(tau * thacc));\n    out[2] = h(th + h(tau * out[3]));"),
+    "f16_unrounded_cosine": ("const double c = h(cos(th));", "const double c = cos(th);"),
     "f64_reset_scale_single": ("ldexp(0.1, -16)", "ldexp((double)0.1f, -16)"),
     "f64_threshold_single": (
         "const double x_limit = 2.4, th_limit = 12.0 * 2.0 * 3.14159265358979323846 / 360.0;",
