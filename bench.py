@@ -1,36 +1,42 @@
 """Benchmark of the batched cart-pole step on one MI355X.
 
-Headline (the JSON line's `value`): 65,536 environments advanced one step
-per kernel launch by the fused step kernel, random actions, each step
-writing obs / reward / done -- the configuration on which the paper's
-fusion comparison is made (unfused per-op chain vs one fused kernel).  A
-"step" of this benchmark is one such launch over the whole batch, replayed
-from the library's HIP graph.
+Headline (the JSON line's `value`): 16,777,216 environments x 100 steps with
+random actions and auto-reset, one fused step kernel launch per step, every
+step writing the full trajectory (obs [4][n] f32, reward [n] f32, done [n]
+u8) to HBM -- the bandwidth-bound streaming workload.  A "step" of this
+benchmark (--steps K, --warmup W) is one whole such rollout (100 launches,
+1.68e9 environment-steps), so `value` is env-steps/s over K rollouts and
+`ms_per_step` the time of one rollout.
 
 Also measured in the same run (extra keys of the same JSON line):
   roofline      HBM roofline of the headline kernel: algorithmic bytes per
-                launch over the mean launch duration (HIP events around the
-                timed region, divided by the launches), and the HBM traffic
-                from stored counter readings while the kernel sources match;
-  unfused, concat, fused_direct
-                the same workload through the one-op-per-kernel chain, split
-                at a concatenation of the updated state (the paper's baseline
-                before "no concat"), and the fused kernel launched from the
-                host step by step; speedups against each, also like for like
-                (every level host-launched);
+                launch over its mean launch duration (HIP events around the
+                timed region on the launch stream, divided by the launches),
+                and its HBM traffic from stored rocprofv3 counter readings
+                while the kernel sources match (null otherwise);
+  launch_bound  65,536 environments x 1,000 steps, one step per launch: the
+                fused step replayed from the library's HIP graph (whether the
+                timed calls replayed is checked), the fused step launched
+                from the host step by step, the step split at a
+                concatenation of the updated state (the paper's baseline
+                before "no concat") and the one-op-per-kernel chain; fusion
+                speedups, also like for like (every level host-launched);
+                warm-ups and repetitions fixed, whatever --steps/--warmup;
   configs       register-resident rollouts (1,024 x 200; 1,048,576 x 1,000 in
-                binary32, binary64 and binary16), 16,777,216 x 100 with the
-                full trajectory (streaming fused steps, and the resident
-                kernel writing the same trajectory), 4,194,304 x 500 with the
-                MLP policy (fused; and as separate kernels on one or two
+                binary32, binary64 and binary16), the resident kernel writing
+                the headline's trajectory, 4,194,304 x 500 with the MLP
+                policy (fused; and as separate kernels on one or two
                 streams), 16 batches x 4,096 stepped by one grouped launch;
   unroll        the resident kernel at k steps per launch (k = 1 ... 1,000);
   references    a plain copy and fill (bandwidth), issue rates per vector
                 instruction class, and the per-node floors of graph replay
-                (reference kernels of libcpref.so);
-  cpu_baseline  the CPU oracle on the host cores (one thread, and all of
-                them), a small-batch sweep against the resident kernel
-                (crossover) and the oracle's rate per configuration.
+                (reference kernels of bench_ref/libcpref.so);
+  cpu_baseline  the CPU oracle on a sample of the headline workload (one
+                thread, and all of them), a small-batch sweep of the three
+                fusion levels against it (crossover) and the oracle's rate
+                per configuration.
+Fields taken from stored counter readings rather than this run say so
+("stored_counters": true, with the profile they come from).
 
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--quick] [--no-cpu]
                        [--only NAME]   (one workload or reference, its JSON only)
@@ -81,7 +87,14 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 # as null until the counters are taken again.
 _CSRC = "paper_2301_13062_amd/csrc/"
 COUNTERS = {
-    # HBM traffic of one headline launch (fused step, 65,536 environments):
+    # HBM traffic of one headline launch (fused streaming step, 16,777,216
+    # environments writing the trajectory): FETCH_SIZE and WRITE_SIZE, KiB
+    # per dispatch (profiles/fused_step_16777216env_hbm.md)
+    "fused_step_16777216": {
+        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_device.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "0000000000000000", "fetch_kib": 188613.5, "write_kib": 435687.5,
+        "profile": "profiles/fused_step_16777216env_hbm.md"},
+    # HBM traffic of one launch-bound launch (fused step, 65,536 environments):
     # FETCH_SIZE and WRITE_SIZE, KiB per dispatch
     "fused_step_65536": {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_device.h", _CSRC + "cp_launch.h"],
@@ -128,6 +141,15 @@ def sources_sha(files):
     return h.hexdigest()[:16]
 
 
+def ref_lib():
+    """The reference kernels' library (bench_ref/), built here if missing."""
+    from bench_ref import build as R
+
+    if not os.path.exists(R.LIB):
+        R.build()
+    return R.LIB
+
+
 def stored_counters(key):
     c = COUNTERS[key]
     return c if sources_sha(c["sources"]) == c["sha256_16"] else None
@@ -149,7 +171,9 @@ def valu_issue(key, env_steps_per_s):
     if c is None:
         return None
     per_cycle = c["valu_per_wave_step"] * env_steps_per_s / 64 / CUS / CLOCK_PEAK_HZ
-    return {"valu_per_wave_step": c["valu_per_wave_step"], "per_cu_per_cycle": per_cycle,
+    return {"reading": "VALU instruction issue / issue peak",
+            "valu_per_wave_step": c["valu_per_wave_step"], "stored_counters": True,
+            "per_cu_per_cycle": per_cycle,
             "peak_per_cu_per_cycle": ISSUE_PEAK_PER_CU_CYCLE,
             "frac": per_cycle / ISSUE_PEAK_PER_CU_CYCLE, "clock_ghz": CLOCK_PEAK_HZ / 1e9}
 
@@ -157,13 +181,15 @@ def valu_issue(key, env_steps_per_s):
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=1000)
-    ap.add_argument("--warmup", type=int, default=2000)
-    ap.add_argument("--quick", action="store_true", help="headline only, no extra configs")
+    ap.add_argument("--steps", type=int, default=10,
+                    help="timed headline rollouts (16,777,216 envs x 100 steps each)")
+    ap.add_argument("--warmup", type=int, default=2, help="untimed headline rollouts first")
+    ap.add_argument("--quick", action="store_true", help="headline only, no extra workloads")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--only", choices=["headline", "resident_1024x200", "resident_1048576x1000",
+    ap.add_argument("--only", choices=["headline", "launch_bound", "launch_bound_fused",
+                                       "resident_1024x200", "resident_1048576x1000",
                                        "resident_f64_1048576x1000", "resident_f16_1048576x1000",
-                                       "streaming_16777216x100", "resident_traj_16777216x100",
+                                       "resident_traj_16777216x100",
                                        "policy_4194304x500",
                                        "policy_separate_4194304x500",
                                        "policy_two_streams_4194304x500", "horizontal_16x4096",
@@ -194,10 +220,46 @@ def timed(fn, reps=1):
     return (time.perf_counter() - t0) * 1e3, e0.elapsed_time(e1)
 
 
-def bench_headline(cp, K, W, legs=("fused", "fused_direct", "concat", "unfused")):
+# The headline workload: the streaming fused step over the full trajectory.
+HEAD_N, HEAD_T = 1 << 24, 100
+
+
+def bench_streaming(cp, K, W):
+    """K timed rollouts of the headline workload after max(W, 1) untimed ones
+    (the first call of a process also pays for loading the kernels).  Every
+    launch is the streaming fused step (each step reads its state from the
+    previous step's obs plane); HIP events bracket the timed region on the
+    stream the library launches on (torch's current stream)."""
     import torch
 
-    n = 65536
+    n, T = HEAD_N, HEAD_T
+    s = cp.CartPoleStates(n, variant=cp.CP_FUSED)
+    cp.cp_init(s, 0)
+    tr = cp.Trajectory(n, T, stats=False, totals=False)
+    for _ in range(max(W, 1)):
+        cp.cp_rollout(s, T, 0, tr)
+    wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=K)
+    out = {"envs": n, "steps_per_rollout": T, "rollouts": K, "wall_ms": wall, "event_ms": ev,
+           "env_steps_per_s": n * T * K / (wall * 1e-3), "ms_per_rollout": wall / K,
+           "kernel_mean_us": ev * 1e3 / (K * T)}
+    del s, tr
+    torch.cuda.empty_cache()
+    return out
+
+
+# Launch-bound workload: 65,536 environments, 1,000 steps of one launch each.
+LB_N, LB_T, LB_REPS = 65536, 1000, 5
+
+
+def bench_launch_bound(cp, legs=("fused", "fused_direct", "concat", "unfused")):
+    """The launch-bound workload at every per-step fusion level, independent
+    of --steps/--warmup: each leg's rollout is warmed up (the graph leg twice:
+    its first call of a kind is recorded, the second builds the graph, and
+    one replay more), then LB_REPS timed calls; the median call is reported.
+    The graph leg checks that every timed call was replayed."""
+    import statistics
+
+    n, T = LB_N, LB_T
     out = {}
     for name, variant, graphs in (("fused", cp.CP_FUSED, True),
                                   ("fused_direct", cp.CP_FUSED, False),
@@ -207,24 +269,45 @@ def bench_headline(cp, K, W, legs=("fused", "fused_direct", "concat", "unfused")
             continue
         s = cp.CartPoleStates(n, variant=variant, graphs=graphs)
         cp.cp_init(s, 0)
-        tr = cp.Trajectory(n, K, stats=False, totals=False)
-        # W warm-up steps as calls of the timed call's shape (K steps into
-        # the same buffers; with graphs, the first such call is recorded
-        # and the second builds the graph that the timed call replays)
-        left = W
-        while left > 0:
-            steps = min(K, left)
-            cp.cp_rollout(s, steps, 0, tr if steps == K else None)
-            left -= steps
-        # the library launches the K step kernels back to back on torch's
-        # current stream (fused: replayed from the HIP graph built during
-        # the warm-up; fused_direct: one host launch per step); HIP
-        # events bracket the whole timed region
-        wall, ev = timed(lambda: cp.cp_rollout(s, K, 0, tr))
-        out[name] = {"wall_ms": wall, "event_ms": ev, "env_steps_per_s": n * K / (wall * 1e-3),
-                     "us_per_step": wall * 1e3 / K, "event_us_per_step": ev * 1e3 / K}
+        tr = cp.Trajectory(n, T, stats=False, totals=False)
+        for _ in range(3 if graphs else 1):
+            cp.cp_rollout(s, T, 0, tr)
+        _sync()
+        before = cp.cp_graph_replays()
+        calls = [timed(lambda: cp.cp_rollout(s, T, 0, tr)) for _ in range(LB_REPS)]
+        replayed = cp.cp_graph_replays() - before
+        if graphs and replayed != LB_REPS:
+            raise RuntimeError(f"graph leg: {replayed} of {LB_REPS} timed calls replayed")
+        wall = statistics.median(c[0] for c in calls)
+        ev = statistics.median(c[1] for c in calls)
+        out[name] = {"us_per_step": wall * 1e3 / T, "event_us_per_step": ev * 1e3 / T,
+                     "env_steps_per_s": n * T / (wall * 1e-3)}
+        if graphs:
+            out[name]["timed_calls_replayed"] = replayed
         del tr
-    return n, out
+    res = {"envs": n, "steps": T, "repetitions": LB_REPS, **out}
+    if len(out) == 4:
+        f, d = out["fused"], out["fused_direct"]
+        res.update({
+            "fusion_speedup": f["env_steps_per_s"] / out["unfused"]["env_steps_per_s"],
+            "no_concat_speedup": f["env_steps_per_s"] / out["concat"]["env_steps_per_s"],
+            "graph_speedup": f["env_steps_per_s"] / d["env_steps_per_s"],
+            # the same ratios with every level launched from the host step
+            # by step (the unfused and concat levels are not graph-replayed)
+            "fusion_speedup_host_launched": d["env_steps_per_s"]
+            / out["unfused"]["env_steps_per_s"],
+            "no_concat_speedup_host_launched": d["env_steps_per_s"]
+            / out["concat"]["env_steps_per_s"],
+        })
+        kern = f["event_us_per_step"]
+        gbs = STEP_BYTES_WITH_OUTPUTS * n / (kern * 1e-6) / 1e9
+        res["roofline"] = {"bound": "launch latency (HBM reported)", "achieved": gbs,
+                           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+                           "bytes_per_env_step": STEP_BYTES_WITH_OUTPUTS,
+                           "traffic": measured_traffic_bytes("fused_step_65536"),
+                           "stored_counters": True,
+                           "kernel_mean_us": kern}
+    return res
 
 
 UNROLL_LADDER = (1, 2, 5, 10, 20, 50, 100, 250, 1000)
@@ -292,9 +375,7 @@ def bench_valu_reference():
 
     import torch
 
-    from paper_2301_13062_amd import build as B
-
-    ref = ctypes.CDLL(B.REF_LIB)
+    ref = ctypes.CDLL(ref_lib())
     ref.cpref_chains.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
                                  ctypes.c_void_p]
     blocks, iters = 256 * 8, 2000  # blocks of 4 waves: 8 waves per SIMD on 256 CUs
@@ -328,9 +409,7 @@ def bench_graph_floor(head_us=None):
 
     import torch
 
-    from paper_2301_13062_amd import build as B
-
-    ref = ctypes.CDLL(B.REF_LIB)
+    ref = ctypes.CDLL(ref_lib())
     ref.cpref_empty.argtypes = [ctypes.c_int, ctypes.c_void_p]
     ref.cpref_touch.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_int64, ctypes.c_void_p]
     n, K = 65536, 1000
@@ -377,8 +456,6 @@ def bench_configs(cp, only=None):
         res["resident_f64_1048576x1000"] = _resident_large(cp, "f64")
     if want("resident_f16_1048576x1000"):
         res["resident_f16_1048576x1000"] = _resident_large(cp, "f16")
-    if want("streaming_16777216x100"):
-        res["streaming_16777216x100"] = _streaming(cp)
     if want("resident_traj_16777216x100"):
         res["resident_traj_16777216x100"] = _resident_traj(cp)
     if want("policy_4194304x500"):
@@ -477,34 +554,18 @@ def _resident_large(cp, precision="f32"):
     mean_ms = ev / 5
     eps = n * T / (mean_ms * 1e-3)
     peak = VALU_PEAK_TOPS / 2 if precision == "f64" else VALU_PEAK_TOPS
+    # Two readings of "VALU utilisation": the useful operation rate (31
+    # operations per env-step against the op-rate peak), and the issue rate
+    # (counter-measured VALU instructions per wave-step at this run's rate,
+    # against two wave64 instructions per CU per cycle at 2.4 GHz).
     out = {"env_steps_per_s": eps, "ms": mean_ms,
-           "roofline": {"bound": "alu", "achieved": eps * STEP_FLOPS / 1e12,
+           "roofline": {"bound": "alu", "reading": "useful operations / op-rate peak",
+                        "achieved": eps * STEP_FLOPS / 1e12,
                         "peak": peak, "unit": "TOP/s",
                         "frac": eps * STEP_FLOPS / 1e12 / peak,
                         "ops_per_env_step": STEP_FLOPS}}
     out["valu_issue"] = valu_issue("resident_1048576x1000" if precision == "f32"
                                    else f"resident_{precision}_1048576x1000", eps)
-    return out
-
-
-def _streaming(cp):
-    import torch
-
-    # 16,777,216 x 100, fused step per launch with full trajectory (HBM-bound)
-    n, T = 1 << 24, 100
-    s = cp.CartPoleStates(n, variant=cp.CP_FUSED)
-    cp.cp_init(s, 0)
-    tr = cp.Trajectory(n, T, stats=False, totals=False)
-    cp.cp_rollout(s, T, 0, tr)
-    wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=3)
-    mean_ms = ev / (3 * T)  # per launch: T back-to-back step kernels per rollout
-    gbs = STEP_BYTES_TRAJ_LARGE * n / (mean_ms * 1e-3) / 1e9
-    out = {"env_steps_per_s": n * T * 3 / (ev * 1e-3), "ms": ev / 3,
-           "kernel_mean_us": mean_ms * 1e3,
-           "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": STEP_BYTES_TRAJ_LARGE}}
-    del s, tr
-    torch.cuda.empty_cache()
     return out
 
 
@@ -553,7 +614,7 @@ def _policy(cp):
                          "unit": "TFLOP/s", "frac": tflops / BF16_MFMA_PEAK_TFLOPS,
                          "flops_per_env_step": POLICY_FLOPS},
             "valu_issue": valu_issue("policy_4194304x500", eps),
-            "mfma_busy_frac": c["mfma_busy"] if c else None}
+            "mfma_busy_frac": c["mfma_busy"] if c else None, "mfma_busy_stored_counters": True}
 
 
 def _policy_separate(cp, streams):
@@ -602,13 +663,16 @@ def _policy_separate(cp, streams):
     return {"env_steps_per_s": n * T / (ms * 1e-3), "ms": ms, "streams": streams}
 
 
-CROSSOVER_N = (1, 4, 16, 64, 256, 1024, 4096)
+CROSSOVER_N = (1, 4, 16, 64, 256, 1024, 2048, 4096)
+CROSSOVER_LEVELS = (("unfused", "CP_UNFUSED", False), ("fused", "CP_FUSED", True),
+                    ("resident", "CP_RESIDENT", False))
 
 
-def _oracle_rate(n, T, workers):
-    """Oracle env-steps/s on n environments x T steps, the environments split
-    over `workers` threads (independent ranges; the C oracle releases the
-    GIL through ctypes)."""
+def _oracle_rate(n, T, workers, min_s=0.2):
+    """Oracle env-steps/s on n environments x T steps (random actions), the
+    environments split over `workers` threads (independent ranges; the C
+    oracle releases the GIL through ctypes); repeated from the start state
+    until at least min_s seconds have passed."""
     from concurrent.futures import ThreadPoolExecutor
 
     import numpy as np
@@ -616,37 +680,51 @@ def _oracle_rate(n, T, workers):
     import oracle as O
 
     parts = [p for p in np.array_split(np.arange(n, dtype=np.uint32), min(workers, n)) if len(p)]
-    states = []
-    for ids in parts:
-        o = O.OracleState(len(ids), ids)
-        O.init(o, 0)
-        states.append(o)
-    t0 = time.perf_counter()
-    with ThreadPoolExecutor(max_workers=len(states)) as ex:
-        list(ex.map(lambda o: O.rollout(o, T), states))
-    return n * T / (time.perf_counter() - t0)
+    done, t0 = 0, time.perf_counter()
+    with ThreadPoolExecutor(max_workers=len(parts)) as ex:
+        while True:
+            states = []
+            for ids in parts:
+                o = O.OracleState(len(ids), ids)
+                O.init(o, 0)
+                states.append(o)
+            list(ex.map(lambda o: O.rollout(o, T), states))
+            done += n * T
+            dt = time.perf_counter() - t0
+            if dt >= min_s:
+                return done / dt
 
 
 def crossover(cp, T=1000):
-    """Small-batch sweep (the paper's CPU/GPU comparison): the register-
-    resident kernel against the CPU oracle on one thread and on the host's
-    cores, N environments x T steps, random actions."""
+    """Small-batch sweep (the paper's CPU/GPU comparison, Sec. "Comparison
+    with Jax CPU implementation"): every fusion level -- the one-op-per-kernel
+    chain, the fused step (one launch per step, replayed from the HIP graph)
+    and the register-resident kernel -- against the CPU oracle on one thread
+    and on the host's cores, N environments x T steps, random actions."""
     workers = min(16, os.cpu_count() or 1)
     rows = {}
     for n in CROSSOVER_N:
-        s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
-        cp.cp_init(s, 0)
-        cp.cp_rollout(s, T, 0, None)
-        wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, None), reps=5)
-        rows[str(n)] = {"gpu": n * T * 5 / (wall * 1e-3), "cpu_1": _oracle_rate(n, T, 1),
-                        "cpu_all": _oracle_rate(n, T, workers)}
-    # the smallest batch from which on the GPU beats the oracle on one
-    # thread and on all workers
+        row = {"cpu_1": _oracle_rate(n, T, 1), "cpu_all": _oracle_rate(n, T, workers)}
+        for name, const, graphs in CROSSOVER_LEVELS:
+            s = cp.CartPoleStates(n, variant=getattr(cp, const), graphs=graphs)
+            cp.cp_init(s, 0)
+            reps = 2 if name == "unfused" else 5
+            for _ in range(3 if graphs else 1):
+                cp.cp_rollout(s, T, 0, None)
+            wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, None), reps=reps)
+            row[name] = n * T * reps / (wall * 1e-3)
+        rows[str(n)] = row
+    # per level, the smallest batch from which on it beats the oracle on one
+    # thread and on all workers (at that batch and every larger one swept)
     ns = sorted(int(k) for k in rows)
-    ahead = [rows[str(k)]["gpu"] > max(rows[str(k)]["cpu_1"], rows[str(k)]["cpu_all"]) for k in ns]
-    faster = [k for i, k in enumerate(ns) if all(ahead[i:])]
+    from_n = {}
+    for name, _, _ in CROSSOVER_LEVELS:
+        ahead = [rows[str(k)][name] > max(rows[str(k)]["cpu_1"], rows[str(k)]["cpu_all"])
+                 for k in ns]
+        faster = [k for i, k in enumerate(ns) if all(ahead[i:])]
+        from_n[name] = min(faster) if faster else None
     return {"steps": T, "cpu_workers": workers, "env_steps_per_s": rows,
-            "gpu_faster_from_n": min(faster) if faster else None}
+            "gpu_faster_from_n": from_n}
 
 
 def config_oracle_rates():
@@ -681,7 +759,6 @@ def config_oracle_rates():
         run("resident_1048576x1000", 1 << 20, 1000, 256),
         run("resident_f64_1048576x1000", 1 << 20, 1000, 256, prec=O.F64),
         run("resident_f16_1048576x1000", 1 << 20, 1000, 256, prec=O.F16),
-        run("streaming_16777216x100", 1 << 24, 100, 256, traj=True),
         run("policy_4194304x500", 1 << 22, 500, 16384, policy=True),
     ])
 
@@ -697,24 +774,76 @@ def _host():
     return {"nproc": os.cpu_count(), "cpu_model": model}
 
 
-def cpu_baseline():
+def cpu_baseline(stride=32, chunk=1 << 16):
+    """The oracle on a sample of the headline workload: every stride-th of its
+    16,777,216 environments (their own global indices, so each behaves as in
+    the full batch) x 100 steps with the full trajectory kept, in chunks of
+    `chunk` environments; once on one thread, once with the chunks spread over
+    the host's cores."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import numpy as np
+
     import oracle as O
 
-    n, T = 65536, 1000
-    o = O.OracleState(n)
-    O.init(o, 0)
+    ids = np.arange(0, HEAD_N, stride, dtype=np.uint32)
+    chunks = [ids[j:j + chunk] for j in range(0, len(ids), chunk)]
+
+    def run(c):
+        o = O.OracleState(len(c), c)
+        O.init(o, 0)
+        O.rollout(o, HEAD_T, traj=True)
+
     t0 = time.perf_counter()
-    O.rollout(o, T, traj=("done",))
-    dt = time.perf_counter() - t0
+    for c in chunks:
+        run(c)
+    dt1 = time.perf_counter() - t0
     workers = min(16, os.cpu_count() or 1)
-    return {"value": n * T / dt, "unit": "env-steps/s", "cores": 1, "kind": "oracle",
-            "sample": f"the whole headline workload ({n} envs x {T} steps, random actions, "
-                      f"done flags kept) on one host thread, {dt:.1f} s",
-            "all_cores": {"value": _oracle_rate(n, T, workers), "unit": "env-steps/s",
-                          "cores": workers,
-                          "sample": "the same workload split over independent environment "
-                                    "ranges, one thread each"},
+    t0 = time.perf_counter()
+    with ThreadPoolExecutor(max_workers=workers) as ex:
+        list(ex.map(run, chunks))
+    dta = time.perf_counter() - t0
+    m = len(ids) * HEAD_T
+    return {"value": m / dt1, "unit": "env-steps/s", "cores": 1, "kind": "oracle",
+            "sample": f"every {stride}th of the headline's {HEAD_N} envs ({len(ids)}) x "
+                      f"{HEAD_T} steps, random actions, obs/reward/done kept, {dt1:.1f} s",
+            "all_cores": {"value": m / dta, "unit": "env-steps/s", "cores": workers,
+                          "sample": f"the same sample in {len(chunks)} chunks of {chunk} envs "
+                                    f"over {workers} threads, {dta:.1f} s"},
             "host": _host()}
+
+
+def headline_line(head, K, W):
+    n, T = head["envs"], head["steps_per_rollout"]
+    kern_us = head["kernel_mean_us"]
+    gbs = STEP_BYTES_TRAJ_LARGE * n / (kern_us * 1e-6) / 1e9
+    c = COUNTERS["fused_step_16777216"]
+    return {
+        "metric": METRIC,
+        "value": head["env_steps_per_s"],
+        "unit": "env-steps/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": W,
+        "ms_per_step": head["ms_per_rollout"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "cart-pole streaming fused step: 16,777,216 envs x 100 steps "
+                               "per rollout (a bench step), one launch per env step, random "
+                               "actions, auto-reset, obs/reward/done trajectory written to HBM "
+                               "every step",
+                   "envs": n, "steps_per_rollout": T, "steps_per_launch": 1, "variant": "fused"},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gbs / HBM_PEAK_GBS,
+                     "traffic": measured_traffic_bytes("fused_step_16777216"),
+                     "traffic_stored_counters": True, "traffic_profile": c["profile"],
+                     "bytes_per_env_step": STEP_BYTES_TRAJ_LARGE,
+                     "kernel": "k_fused_step<false, false, true, true>",
+                     "kernel_mean_us": kern_us, "launches_timed": K * T},
+    }
 
 
 def main():
@@ -724,17 +853,23 @@ def main():
               "environment index without communication, so a multi-GPU figure is not measured "
               "here.", file=sys.stderr)
         sys.exit(2)
+    K, W = args.steps, args.warmup
+    if K < 1 or W < 0:
+        print("--steps must be >= 1 and --warmup >= 0", file=sys.stderr)
+        sys.exit(2)
     import torch
 
     import paper_2301_13062_amd as cp
 
     cp.lib()  # fails loudly without the built library
     assert torch.cuda.is_available(), "no HIP device"
-    K, W = args.steps, args.warmup
     if args.only == "headline":
-        # the headline's fused leg alone (graph replay after the warm-up)
-        n, head = bench_headline(cp, K, W, legs=("fused",))
-        print(json.dumps({"only": "headline", **head["fused"]}))
+        print(json.dumps({"only": "headline", **bench_streaming(cp, K, W)}))
+        return
+    if args.only in ("launch_bound", "launch_bound_fused"):
+        legs = ("fused",) if args.only == "launch_bound_fused" else None
+        res = bench_launch_bound(cp, legs) if legs else bench_launch_bound(cp)
+        print(json.dumps({"only": args.only, **res}))
         return
     if args.only:
         refs = {"copy": bench_copy, "fill": bench_fill, "valu_reference": bench_valu_reference,
@@ -743,53 +878,16 @@ def main():
         print(json.dumps({"only": args.only, **res}))
         return
 
-    n, head = bench_headline(cp, K, W)
-    fused = head["fused"]
-    kern_us = fused["event_us_per_step"]
-    gbs = STEP_BYTES_WITH_OUTPUTS * n / (kern_us * 1e-6) / 1e9
-    line = {
-        "metric": METRIC,
-        "value": fused["env_steps_per_s"],
-        "unit": "env-steps/s",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": W,
-        "ms_per_step": fused["wall_ms"] / K,
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": "cart-pole fused step kernel, 65,536 envs, 1 step per launch, "
-                               "random actions, obs/reward/done written every step",
-                   "envs": n, "steps_per_launch": 1, "variant": "fused"},
-        "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gbs / HBM_PEAK_GBS,
-                     "traffic": measured_traffic_bytes("fused_step_65536"),
-                     "bytes_per_env_step": STEP_BYTES_WITH_OUTPUTS,
-                     "kernel_mean_us": kern_us},
-        "unfused": {"env_steps_per_s": head["unfused"]["env_steps_per_s"],
-                    "us_per_step": head["unfused"]["us_per_step"]},
-        "fusion_speedup": fused["env_steps_per_s"] / head["unfused"]["env_steps_per_s"],
-        "concat": {"env_steps_per_s": head["concat"]["env_steps_per_s"],
-                   "us_per_step": head["concat"]["us_per_step"]},
-        "no_concat_speedup": fused["env_steps_per_s"] / head["concat"]["env_steps_per_s"],
-        "fused_direct": {"env_steps_per_s": head["fused_direct"]["env_steps_per_s"],
-                         "us_per_step": head["fused_direct"]["us_per_step"]},
-        "graph_speedup": fused["env_steps_per_s"] / head["fused_direct"]["env_steps_per_s"],
-        # the same ratios with every level launched from the host step by step
-        # (the unfused and concat levels are not graph-replayed)
-        "fusion_speedup_host_launched": head["fused_direct"]["env_steps_per_s"]
-        / head["unfused"]["env_steps_per_s"],
-        "no_concat_speedup_host_launched": head["fused_direct"]["env_steps_per_s"]
-        / head["concat"]["env_steps_per_s"],
-    }
+    head = bench_streaming(cp, K, W)
+    line = headline_line(head, K, W)
     if not args.quick:
+        lb = bench_launch_bound(cp)
+        line["launch_bound"] = lb
         line["configs"] = bench_configs(cp)
         line["unroll"] = bench_unroll(cp)
         line["references"] = {"copy": bench_copy(), "fill": bench_fill(),
                               "valu": bench_valu_reference(),
-                              "graph_floor": bench_graph_floor(kern_us)}
+                              "graph_floor": bench_graph_floor(lb["fused"]["event_us_per_step"])}
     if not args.no_cpu:
         line["cpu_baseline"] = cpu_baseline()
         if not args.quick:

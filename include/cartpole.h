@@ -27,9 +27,13 @@
  *    stream).  Results are visible after the caller synchronises it.
  *  - Return value: CP_OK (0) or a negative CP_ERR_* code; cp_last_error()
  *    then gives a message (per calling thread).  Arguments are validated
- *    before any HIP call: on CP_ERR_NULL/SIZE/ALIGN/RANGE/UNSUPPORTED nothing
- *    is launched and *s is unchanged.  CP_ERR_HIP reports a failed launch.
- *  - Outputs must not overlap the state arrays or each other.
+ *    before any HIP call: on CP_ERR_NULL/SIZE/ALIGN/RANGE/UNSUPPORTED/OVERLAP
+ *    nothing is launched and *s is unchanged.  CP_ERR_HIP reports a failed
+ *    launch.
+ *  - Outputs must not overlap the state arrays or each other: cp_step and
+ *    cp_rollout compare the byte ranges of every output they are given with
+ *    those of the state arrays and of the other outputs, and return
+ *    CP_ERR_OVERLAP when two share a byte.
  *  - A cp_states handle is not thread-safe; distinct handles are independent.
  */
 #ifndef CARTPOLE_H
@@ -57,6 +61,7 @@ extern "C" {
 #define CP_ERR_RANGE (-4)       /* step counter or environment index would overflow   */
 #define CP_ERR_HIP (-5)         /* a HIP launch failed; see cp_last_error()           */
 #define CP_ERR_UNSUPPORTED (-6) /* combination not provided (e.g. policy + UNFUSED)    */
+#define CP_ERR_OVERLAP (-7)     /* an output shares memory with the state or another output */
 
 /* Precision of the state, the step and the obs trajectory
  * (cp_states.precision).  The paper's own implementation is binary32; the
@@ -204,6 +209,28 @@ int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
  * error).                                                                  */
 int cp_policy(const float *obs, int64_t n, const uint16_t *policy_w, uint8_t *actions,
               void *stream);
+
+/* Host-side generator of MLP policy weights (the network of the simulation
+ * fused with inference, Sec. "Future Work"): fills host_w[0 .. 4479] with
+ * the bf16 bit patterns of W1[4][64], W2[64][64], W3[64][2] (row-major
+ * [in][out], concatenated) drawn N(0, 1/fan_in) from `seed`, fan_in = 4, 64,
+ * 64.  Weight q (0 <= q < 4480, in that order) is a Box-Muller normal
+ * (Box and Muller, 1958) from one Threefry-2x32-20 output (a, b) on counter
+ * (q, 0) under the stream key of `seed` with tag 3 (the key derivation of
+ * the action and reset streams):
+ *     u1 = (a + 1/2) 2^-32,  u2 = (b + 1/2) 2^-32,
+ *     z  = sqrt(-2 ln u1) cos((2 pi) u2)          (binary64, the C library)
+ *     w  = z / sqrt(fan_in)                       (exact: a power of two)
+ * rounded to binary32 and then to bfloat16, to nearest with ties to even at
+ * both steps.  Host memory only, no HIP call, no allocation; the caller
+ * copies the array to the device for cp_states.policy_w / cp_policy.
+ * Returns CP_OK or CP_ERR_NULL (host_w NULL).                              */
+int cp_policy_init(uint16_t *host_w, uint64_t seed);
+
+/* Number of cp_rollout calls in this process whose steps were replayed from
+ * a cached HIP graph (CP_FUSED with a workspace, above), for callers and
+ * benchmarks that need to know which launch path ran.  Thread-safe.        */
+uint64_t cp_graph_replays(void);
 
 /* Bytes of workspace a variant takes for n environments: needed by
  * CP_UNFUSED and CP_CONCAT, optional for CP_FUSED (graph replay; 0 from

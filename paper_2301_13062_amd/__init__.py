@@ -17,8 +17,8 @@ import torch
 
 CP_UNFUSED, CP_FUSED, CP_RESIDENT, CP_CONCAT = 0, 1, 2, 3
 VARIANTS = {"unfused": CP_UNFUSED, "fused": CP_FUSED, "resident": CP_RESIDENT, "concat": CP_CONCAT}
-CP_OK, CP_ERR_NULL, CP_ERR_SIZE, CP_ERR_ALIGN, CP_ERR_RANGE, CP_ERR_HIP, CP_ERR_UNSUPPORTED = (
-    0, -1, -2, -3, -4, -5, -6)
+(CP_OK, CP_ERR_NULL, CP_ERR_SIZE, CP_ERR_ALIGN, CP_ERR_RANGE, CP_ERR_HIP, CP_ERR_UNSUPPORTED,
+ CP_ERR_OVERLAP) = (0, -1, -2, -3, -4, -5, -6, -7)
 CP_POLICY_WEIGHTS = 4480
 CP_PREC_F32, CP_PREC_F64, CP_PREC_F16 = 0, 1, 2
 PRECISIONS = {"f32": CP_PREC_F32, "f64": CP_PREC_F64, "f16": CP_PREC_F16}
@@ -77,6 +77,10 @@ def lib():
         L.cp_step_group.restype = ctypes.c_int
         L.cp_policy.argtypes = [_p, ctypes.c_int64, _p, _p, _p]
         L.cp_policy.restype = ctypes.c_int
+        L.cp_policy_init.argtypes = [_p, ctypes.c_uint64]
+        L.cp_policy_init.restype = ctypes.c_int
+        L.cp_graph_replays.argtypes = []
+        L.cp_graph_replays.restype = ctypes.c_uint64
         L.cp_workspace_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32]
         L.cp_workspace_bytes.restype = ctypes.c_size_t
         L.cp_last_error.argtypes = []
@@ -210,6 +214,21 @@ def cp_policy(obs, policy_w, actions, stream=None) -> None:
     assert obs.shape == (4, n) and obs.dtype == torch.float32 and obs.is_contiguous()
     st = stream if stream is not None else torch.cuda.current_stream()
     _check(lib().cp_policy(_ptr(obs), n, _ptr(policy_w), _ptr(actions), st.cuda_stream))
+
+
+def cp_policy_init(seed: int):
+    """The library's host-side weight generator: a uint16 numpy array of the
+    4480 bf16 bit patterns (W1, W2, W3) drawn from `seed` (cartpole.h)."""
+    import numpy as np
+
+    w = np.empty(CP_POLICY_WEIGHTS, dtype=np.uint16)
+    _check(lib().cp_policy_init(w.ctypes.data, int(seed)))
+    return w
+
+
+def cp_graph_replays() -> int:
+    """cp_rollout calls replayed from cached HIP graphs so far in this process."""
+    return int(lib().cp_graph_replays())
 
 
 def cp_workspace_bytes(n: int, variant: int) -> int:

@@ -10,10 +10,6 @@ OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(OUT_DIR, "libcartpole.so")
 
 SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip"]
-# Measurement references (issue rates by instruction class, per-launch floors
-# of graph replay), in a library of their own that only the benchmark loads.
-REF_SOURCES = ["ref_valu.hip", "ref_latency.hip"]
-REF_LIB = os.path.join(OUT_DIR, "libcpref.so")
 # A plain C client of the ABI (cartpole.h and the HIP runtime API only), built
 # with the host C compiler; the GPU tests run it.
 CLIENT_SRC = os.path.join(ROOT, "tests", "capi_client.c")
@@ -63,7 +59,6 @@ def _client(verbose):
 def build(verbose=False) -> str:
     os.makedirs(OUT_DIR, exist_ok=True)
     _hipcc(SOURCES, LIB, verbose)
-    _hipcc(REF_SOURCES, REF_LIB, verbose)
     _client(verbose)
     return LIB
 

@@ -1,6 +1,7 @@
 // cp_capi.hip -- the C ABI of libcartpole.so (declared in cartpole.h):
 // argument validation (finished before any HIP call), stream-key
 // derivation, fusion-level dispatch and error reporting.
+#include <cmath>
 #include <cstdarg>
 #include <cstdint>
 #include <cstdio>
@@ -108,6 +109,48 @@ int hip_status(hipError_t e, const char *what) {
   return CP_OK;
 }
 
+// Byte ranges for the overlap checks: [lo, hi), computed in 128 bits so that
+// no product of a length and a count can wrap.
+struct Range {
+  unsigned __int128 lo, hi;
+  const char *name;
+};
+
+Range range_of(const void *p, unsigned __int128 bytes, const char *name) {
+  const unsigned __int128 lo = reinterpret_cast<uintptr_t>(p);
+  return Range{lo, lo + bytes, name};
+}
+
+// The state arrays of a handle (6 ranges).
+int state_ranges(const cp_states *s, Range *out) {
+  const unsigned __int128 n = uint64_t(s->n), eb = elem_bytes(s->precision);
+  out[0] = range_of(s->x, n * eb, "x");
+  out[1] = range_of(s->x_dot, n * eb, "x_dot");
+  out[2] = range_of(s->theta, n * eb, "theta");
+  out[3] = range_of(s->theta_dot, n * eb, "theta_dot");
+  out[4] = range_of(s->ep_index, n * 4u, "ep_index");
+  out[5] = range_of(s->ep_len, n * 4u, "ep_len");
+  return 6;
+}
+
+// CP_ERR_OVERLAP unless every output range is disjoint from every state
+// range and from every other output range.
+int check_overlap(const cp_states *s, const Range *outs, int n_outs) {
+  Range st[6];
+  const int n_st = state_ranges(s, st);
+  auto meet = [](const Range &a, const Range &b) { return a.lo < b.hi && b.lo < a.hi; };
+  for (int i = 0; i < n_outs; ++i) {
+    for (int j = 0; j < n_st; ++j)
+      if (meet(outs[i], st[j]))
+        return fail(CP_ERR_OVERLAP, "output %s overlaps the state array %s", outs[i].name,
+                    st[j].name);
+    for (int j = 0; j < i; ++j)
+      if (meet(outs[i], outs[j]))
+        return fail(CP_ERR_OVERLAP, "outputs %s and %s overlap", outs[j].name, outs[i].name);
+  }
+  return CP_OK;
+}
+
 cp::StepParams step_params(const cp_states *s, uint64_t act_seed) {
   cp::StepParams p{};
   p.xi = p.x = s->x;
@@ -156,6 +199,15 @@ CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *rewa
   if (int e = check_workspace(s)) return e;
   if ((obs && !aligned_to(obs, elem_bytes(s->precision))) || (reward && !aligned4(reward)))
     return fail(CP_ERR_ALIGN, "obs must be aligned to its elements, reward to 4 bytes");
+  {
+    const unsigned __int128 n = uint64_t(s->n);
+    Range outs[3];
+    int k = 0;
+    if (obs) outs[k++] = range_of(obs, 4u * n * elem_bytes(s->precision), "obs");
+    if (reward) outs[k++] = range_of(reward, 4u * n, "reward");
+    if (done) outs[k++] = range_of(done, n, "done");
+    if (int e = check_overlap(s, outs, k)) return e;
+  }
   hipStream_t st = static_cast<hipStream_t>(s->stream);
   const bool policy = s->policy_w && !actions;
   if (policy && s->variant != CP_RESIDENT)
@@ -269,6 +321,19 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
       (tr.global && (reinterpret_cast<uintptr_t>(tr.global) & 7u)))
     return fail(CP_ERR_ALIGN,
                 "trajectory outputs must be aligned to their elements (global: 8-byte)");
+  {
+    const unsigned __int128 n = uint64_t(s->n), T = uint64_t(n_steps);
+    Range outs[7];
+    int k = 0;
+    if (tr.obs && T) outs[k++] = range_of(tr.obs, T * 4u * n * elem_bytes(s->precision), "obs");
+    if (tr.reward && T) outs[k++] = range_of(tr.reward, T * n * 4u, "reward");
+    if (tr.done && T) outs[k++] = range_of(tr.done, T * n, "done");
+    if (tr.done_count) outs[k++] = range_of(tr.done_count, n * 4u, "done_count");
+    if (tr.total_reward) outs[k++] = range_of(tr.total_reward, n * 4u, "total_reward");
+    if (tr.ret_sum) outs[k++] = range_of(tr.ret_sum, n * 4u, "ret_sum");
+    if (tr.global) outs[k++] = range_of(tr.global, 16u, "global");
+    if (int e = check_overlap(s, outs, k)) return e;
+  }
   if (s->policy_w && s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "the MLP policy runs in the CP_RESIDENT variant only");
   if (int e = check_precision_step(s, false)) return e;
@@ -389,6 +454,41 @@ CP_API int cp_policy(const float *obs, int64_t n, const uint16_t *policy_w, uint
     return e;
   return ok();
 }
+
+namespace {
+
+// Binary64 -> binary32 -> bfloat16 bit pattern, to nearest with ties to even
+// at both steps (the conversion to float is IEEE round to nearest).
+uint16_t bf16_of(double v) {
+  const float f = static_cast<float>(v);
+  uint32_t u;
+  static_assert(sizeof u == sizeof f, "binary32");
+  __builtin_memcpy(&u, &f, sizeof u);
+  if ((u & 0x7F800000u) == 0x7F800000u) return uint16_t(u >> 16);  // inf / nan kept as is
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return uint16_t(u >> 16);
+}
+
+constexpr uint32_t kTagWeights = 3u;
+
+}  // namespace
+
+CP_API int cp_policy_init(uint16_t *host_w, uint64_t seed) {
+  if (!host_w) return fail(CP_ERR_NULL, "host_w is NULL");
+  const cp::U2 key = cp::stream_key(seed, kTagWeights);
+  const double two_pi = 2.0 * M_PI, scale = 0x1p-32;
+  for (uint32_t q = 0; q < uint32_t(CP_POLICY_WEIGHTS); ++q) {
+    // fan_in 4 for W1 (the first 4 x 64 weights), 64 for W2 and W3
+    const double inv_sqrt_fan_in = q < 4u * 64u ? 0.5 : 0.125;
+    const cp::U2 r = cp::threefry2x32(key.a, key.b, q, 0u);
+    const double u1 = (double(r.a) + 0.5) * scale, u2 = (double(r.b) + 0.5) * scale;
+    const double z = std::sqrt(-2.0 * std::log(u1)) * std::cos(two_pi * u2);
+    host_w[q] = bf16_of(z * inv_sqrt_fan_in);
+  }
+  return ok();
+}
+
+CP_API uint64_t cp_graph_replays(void) { return cp::graph_replays(); }
 
 CP_API size_t cp_workspace_bytes(int64_t n, int32_t variant) {
   if (n < 1 || n > INT32_MAX) return 0;

@@ -86,6 +86,8 @@ hipError_t launch_fused_step(const StepParams &p, hipStream_t stream);
 // graph cache full: *used says whether the steps were launched.
 hipError_t launch_fused_graph(const StepParams &base, uint32_t T, void *workspace,
                               hipStream_t stream, bool *used);
+// Rollouts replayed from graphs so far in this process.
+uint64_t graph_replays();
 // Register-resident rollout; with p.policy_w set the MLP policy chooses the
 // actions (launch_resident_policy), otherwise the random action stream.
 hipError_t launch_resident(const RolloutParams &p, hipStream_t stream);

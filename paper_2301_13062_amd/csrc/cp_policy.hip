@@ -206,7 +206,9 @@ __global__ __launch_bounds__(kResidentBlock) void k_policy_actions(
        base += gridDim.x * kResidentBlock) {
     const uint32_t i = base + threadIdx.x;
     const uint32_t ic = i < n ? i : n - 1u;
-    const State s{obs[ic], obs[n + ic], obs[2u * n + ic], obs[3u * n + ic]};
+    // plane offsets in 64 bits: 3n passes 2^32 from n > 1,431,655,765
+    const size_t m = n;
+    const State s{obs[ic], obs[m + ic], obs[2u * m + ic], obs[3u * m + ic]};
     const uint32_t a = policy(0u, 0u, s);
     if (i < n) actions[i] = uint8_t(a);
   }

@@ -6,8 +6,12 @@
 //
 // Arithmetic contract (compiled with -ffp-contract=off):
 //   binary64 -- every operation rounded once in binary64, in the operation
-//     order of the binary32 step; divisions are IEEE divisions; sin and cos
-//     are the device library's binary64 routines.
+//     order of the binary32 step; the three divisions by the total mass M are
+//     the product with RN(1/M) corrected once with the exact residual
+//     (Markstein: the correctly rounded quotient away from underflow), the
+//     angular-acceleration division is the IEEE division; sin and cos are
+//     Taylor polynomials on |theta| <= 1/4 (within an ulp) and the device
+//     library's binary64 routines beyond.
 //   binary16 -- constants rounded once from their exact values; additions,
 //     subtractions and products are binary16 instructions (one rounding
 //     each); a quotient is the binary32 quotient rounded once to binary16,

@@ -14,6 +14,7 @@
 // Resident rollout with random actions (paper Sec. "Fusion via Unroll" and
 // Sec. "Comparison with CUDA implementation": all steps in one kernel): the
 // loop itself is shared with the MLP-policy kernel (cp_resident.h).
+#include <atomic>
 #include <mutex>
 #include <vector>
 
@@ -311,6 +312,7 @@ struct RolloutGraph {
 };
 
 std::mutex g_graph_mutex;
+std::atomic<uint64_t> g_replays{0};
 std::vector<RolloutGraph> g_graphs;
 std::vector<RolloutKey> g_seen;  // kinds met once, oldest first
 
@@ -495,8 +497,11 @@ hipError_t launch_fused_graph(const StepParams &base, uint32_t T, void *workspac
   if (e != hipSuccess) return e;
   e = hipGraphLaunch(exec, stream);
   *used = e == hipSuccess;
+  if (*used) g_replays.fetch_add(1u, std::memory_order_relaxed);
   return e;
 }
+
+uint64_t graph_replays() { return g_replays.load(std::memory_order_relaxed); }
 
 size_t concat_workspace_bytes(uint32_t n) { return size_t(n) * sizeof(f32x4); }
 

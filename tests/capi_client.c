@@ -5,9 +5,15 @@
  *     same final states, episode counters and trajectories for one rollout;
  *   - cp_step called n times equals one cp_rollout of n steps;
  *   - cp_step_group on two batches equals cp_step on each;
+ *   - the MLP policy with weights from cp_policy_init (no other source of
+ *     weights): the fused policy rollout equals cp_policy + cp_step per
+ *     step (simulation and inference as separate kernels);
  * and that a bad call returns its error code with a message.  Prints "ok"
  * and returns 0 on success; prints the failed check and returns 1
- * otherwise.  Built by the package build; run by tests/test_gpu_capi_client.py. */
+ * otherwise.  With a file name as argument it also writes the policy
+ * rollout there (done flags [TP][NP] u8, then x, x_dot, theta, theta_dot
+ * [NP] f32 and ep_index, ep_len [NP] u32), for the test to compare with the
+ * oracle.  Built by the package build; run by tests/test_gpu_capi_client.py. */
 #include <hip/hip_runtime_api.h>
 #include <stdint.h>
 #include <stdio.h>
@@ -18,6 +24,9 @@
 
 #define N 3000
 #define T 130
+/* policy rollout: weights of seed 0, states of seed 0, actions from the policy */
+#define NP 2048
+#define TP 100
 
 #define CHECK(cond, what)                                       \
     do {                                                        \
@@ -81,7 +90,15 @@ static int same_state(const run_t *a, const run_t *b, int64_t n) {
            same(a->s.ep_index, b->s.ep_index, n * 4) && same(a->s.ep_len, b->s.ep_len, n * 4);
 }
 
-int main(void) {
+static int save(FILE *f, const void *d, size_t bytes) {
+    void *h = malloc(bytes);
+    (void)hipMemcpy(h, d, bytes, hipMemcpyDeviceToHost);
+    const int ok = fwrite(h, 1, bytes, f) == bytes;
+    free(h);
+    return ok;
+}
+
+int main(int argc, char **argv) {
     const int32_t levels[4] = {CP_UNFUSED, CP_CONCAT, CP_FUSED, CP_RESIDENT};
     run_t run[4];
     for (int v = 0; v < 4; ++v) {
@@ -129,6 +146,46 @@ int main(void) {
     CHECK(same_state(&g[0], &r[0], 1000) && same_state(&g[1], &r[1], 77) && g[0].s.t == 20 &&
               g[1].s.t == 20,
           "cp_step_group equals cp_step on each member");
+
+    /* the MLP policy, weights from the library's host generator */
+    static uint16_t hw[CP_POLICY_WEIGHTS];
+    CHECK(cp_policy_init(hw, 0) == CP_OK, "cp_policy_init");
+    uint16_t *dw = (uint16_t *)dev(sizeof hw);
+    CHECK(hipMemcpy(dw, hw, sizeof hw, hipMemcpyHostToDevice) == hipSuccess, "weights copied");
+    run_t pf, ps;
+    make(&pf, CP_RESIDENT, NP, 0);
+    make(&ps, CP_FUSED, NP, 0);
+    pf.s.policy_w = dw;
+    CHECK(cp_init(&pf.s, 0) == CP_OK && cp_init(&ps.s, 0) == CP_OK, "cp_init");
+    cp_traj tf = {NULL, NULL, pf.done, NULL, NULL, NULL, NULL};
+    CHECK(cp_rollout(&pf.s, TP, 0, &tf) == CP_OK, "policy rollout");
+    /* separate kernels: the policy on the current state planes, then a step
+       with those actions writing the next state planes */
+    float *cur = (float *)dev((size_t)4 * NP * 4);
+    const float *planes[4] = {ps.s.x, ps.s.x_dot, ps.s.theta, ps.s.theta_dot};
+    for (int c = 0; c < 4; ++c)
+        CHECK(hipMemcpy(cur + (size_t)c * NP, planes[c], (size_t)NP * 4,
+                        hipMemcpyDeviceToDevice) == hipSuccess,
+              "state planes copied");
+    uint8_t *act = (uint8_t *)dev(NP);
+    for (int j = 0; j < TP; ++j) {
+        float *nxt = ps.obs + (size_t)j * 4 * NP;
+        CHECK(cp_policy(cur, NP, dw, act, NULL) == CP_OK, "cp_policy");
+        CHECK(cp_step(&ps.s, act, nxt, NULL, ps.done + (size_t)j * NP) == CP_OK, "cp_step");
+        cur = nxt;
+    }
+    CHECK(hipDeviceSynchronize() == hipSuccess, "policy rollouts ran");
+    CHECK(same_state(&pf, &ps, NP) && same(pf.done, ps.done, (size_t)TP * NP),
+          "fused policy rollout equals cp_policy + cp_step");
+    if (argc > 1) {
+        FILE *f = fopen(argv[1], "wb");
+        CHECK(f != NULL, "output file opened");
+        int ok = save(f, pf.done, (size_t)TP * NP);
+        const void *arrs[6] = {pf.s.x, pf.s.x_dot, pf.s.theta, pf.s.theta_dot, pf.s.ep_index,
+                               pf.s.ep_len};
+        for (int c = 0; c < 6; ++c) ok = ok && save(f, arrs[c], (size_t)NP * 4);
+        CHECK(fclose(f) == 0 && ok, "policy rollout written");
+    }
 
     /* an invalid call: an error code and a message, nothing changed */
     cp_states bad = a.s;

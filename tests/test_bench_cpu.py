@@ -55,3 +55,30 @@ def test_peaks_and_algorithmic_figures():
     assert bench.STEP_BYTES_TRAJ_RESIDENT == 16 + 4 + 1
     assert bench.POLICY_FLOPS == 2 * (4 * 64 + 64 * 64 + 64 * 2)
     json.dumps(bench.COUNTERS)  # plain data
+    assert bench.HEAD_N == 1 << 24 and bench.HEAD_T == 100
+    assert bench.COUNTERS["fused_step_16777216"]["profile"].startswith("profiles/")
+
+
+def test_headline_line_shape():
+    # the JSON line built from a headline measurement: the metric's fields,
+    # the streaming workload in config, the roofline of the streaming kernel
+    head = {"envs": 1 << 24, "steps_per_rollout": 100, "rollouts": 20, "wall_ms": 260.0,
+            "event_ms": 255.0, "env_steps_per_s": (1 << 24) * 100 * 20 / 0.26,
+            "ms_per_rollout": 13.0, "kernel_mean_us": 127.5}
+    line = bench.headline_line(head, 20, 5)
+    assert line["value"] == head["env_steps_per_s"] and line["unit"] == "env-steps/s"
+    assert line["steps"] == 20 and line["warmup"] == 5 and line["n_gpus"] == 1
+    assert line["ms_per_step"] == 13.0 and line["dtype"] == "f32"
+    assert "16,777,216 envs x 100 steps" in line["config"]["workload"]
+    r = line["roofline"]
+    assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
+    assert r["achieved"] == pytest.approx(45 * (1 << 24) / 127.5e-6 / 1e9)
+    assert r["frac"] == pytest.approx(r["achieved"] / 8000.0)
+    assert r["launches_timed"] == 2000
+    json.dumps(line)
+
+
+def test_bad_step_counts_are_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "0"],
+                       capture_output=True, text=True, timeout=120)
+    assert r.returncode == 2 and "--steps" in r.stderr and r.stdout == ""

@@ -39,9 +39,10 @@ def test_library_exports_every_declared_symbol():
 def test_reference_library_is_separate():
     # the issue-rate reference kernels live in their own library, which only
     # the benchmark loads; the cart-pole library exports none of it
-    from paper_2301_13062_amd import build as B
+    from bench_ref import build as R
 
-    out = subprocess.run(["nm", "-D", "--defined-only", B.REF_LIB], capture_output=True,
+    assert not os.path.dirname(R.LIB).startswith(os.path.join(ROOT, "paper_2301_13062_amd"))
+    out = subprocess.run(["nm", "-D", "--defined-only", R.LIB], capture_output=True,
                          text=True, check=True).stdout
     assert sorted(set(re.findall(r"\bT (\w+)", out))) == ["cpref_chains", "cpref_empty",
                                                             "cpref_ops_per_iter", "cpref_touch"]
@@ -296,3 +297,110 @@ def test_plain_c_client_is_built_and_links():
     out = subprocess.run(["ldd", B.CLIENT], capture_output=True, text=True, check=True).stdout
     lib = [ln for ln in out.splitlines() if "libcartpole.so" in ln]
     assert lib and "not found" not in lib[0] and os.path.dirname(B.CLIENT) in lib[0], out
+
+
+# --------------------------------------------------------------------------- output overlap
+# Handles from handle(): n = 1000 binary32 environments, state arrays at
+# A + 0x1000 j (4,000 bytes each).  Calls that pass the overlap check are made
+# to fail the next validation step instead (an MLP policy under CP_FUSED), so
+# nothing launches.
+FAR = A + 0x1000000
+
+
+def test_step_outputs_overlapping_the_state_are_refused():
+    L = cp.lib()
+    for obs, rew, done in [(A, None, None),                      # obs over x
+                           (None, A + 0x4000 + 3996, None),      # reward on ep_index's last element
+                           (None, None, A + 0x5000 + 3999),      # done on ep_len's last byte
+                           (A + 0x1000 - 16000 + 4, None, None)]:  # obs's tail over x_dot
+        h = handle()
+        assert L.cp_step(ctypes.byref(h), None, obs, rew, done) == cp.CP_ERR_OVERLAP
+        assert "overlaps the state" in cp.lib().cp_last_error().decode() and h.t == 7
+
+
+def test_step_outputs_overlapping_each_other_are_refused():
+    L = cp.lib()
+    h = handle()
+    # obs [4][1000] f32 = 16,000 bytes; reward on its last element
+    assert L.cp_step(ctypes.byref(h), None, FAR, FAR + 16000 - 4, None) == cp.CP_ERR_OVERLAP
+    assert L.cp_step(ctypes.byref(h), None, None, FAR, FAR + 3999) == cp.CP_ERR_OVERLAP
+    # adjacent ranges share no byte: the call gets as far as the next check
+    h = handle(policy_w=A + 0x900000)
+    assert L.cp_step(ctypes.byref(h), None, FAR, FAR + 16000, FAR + 20000) == cp.CP_ERR_UNSUPPORTED
+    # done just past ep_len's last byte, obs just before x
+    assert L.cp_step(ctypes.byref(h), None, A - 16000, None, A + 0x5000 + 4000) == \
+        cp.CP_ERR_UNSUPPORTED
+
+
+def test_rollout_outputs_overlapping_are_refused():
+    T, n = 10, 1000
+    obs_bytes = T * 4 * n * 4
+
+    def go(**kw):
+        fields = dict(obs=None, reward=None, done=None, done_count=None, total_reward=None,
+                      ret_sum=None)
+        fields["global"] = None
+        fields.update(kw)
+        tr = cp.cp_traj(*[fields[f] for f, _ in cp.cp_traj._fields_])
+        return call_rollout(handle(policy_w=A + 0x900000), T, tr)
+
+    assert go(obs=A + 0x5000 - obs_bytes + 4) == cp.CP_ERR_OVERLAP   # obs's last rows over ep_len
+    assert go(done=A + 0x3000 + 100) == cp.CP_ERR_OVERLAP           # done over theta_dot
+    assert go(obs=FAR, reward=FAR + obs_bytes - 4) == cp.CP_ERR_OVERLAP
+    assert go(reward=FAR, done_count=FAR + T * n * 4 - 4) == cp.CP_ERR_OVERLAP
+    assert go(ret_sum=FAR, **{"global": FAR + 3992}) == cp.CP_ERR_OVERLAP
+    assert go(total_reward=FAR, ret_sum=FAR) == cp.CP_ERR_OVERLAP
+    # the whole trajectory laid out back to back: no overlap, next check fails
+    assert go(obs=FAR, reward=FAR + obs_bytes, done=FAR + obs_bytes + T * n * 4,
+              done_count=FAR + 0x100000, total_reward=FAR + 0x101000, ret_sum=FAR + 0x102000,
+              **{"global": FAR + 0x103000}) == cp.CP_ERR_UNSUPPORTED
+
+
+def test_overlap_ranges_do_not_wrap():
+    # 2^31 - 1 environments x 2^31 - 1 steps of binary64 obs is about 2^67
+    # bytes: the range check must not wrap around to a small length
+    h = handle(n=2 ** 31 - 1, x=A, x_dot=A + (1 << 36), theta=A + (2 << 36),
+               theta_dot=A + (3 << 36), ep_index=A + (4 << 36), ep_len=A + (5 << 36),
+               variant=cp.CP_RESIDENT, precision=cp.CP_PREC_F64, t=0)
+    tr = cp.cp_traj(A - (1 << 40), None, None, None, None, None, None)
+    assert cp.lib().cp_rollout(ctypes.byref(h), 2 ** 31 - 1, 0, ctypes.byref(tr)) == \
+        cp.CP_ERR_OVERLAP
+
+
+# --------------------------------------------------------------------------- weights
+@pytest.mark.parametrize("seed", [0, 1, 7, 2 ** 40 + 5, 2 ** 64 - 1])
+def test_policy_init_equals_the_seeded_input_definition(seed):
+    # the library's host generator and the seeded-input module implement the
+    # same published definition (Threefry-2x32-20 on counter (q, 0), Box-Muller
+    # in binary64, binary32 then bf16 rounding) independently: bit for bit
+    import numpy as np
+
+    from paper_2301_13062_amd import synth
+
+    w = cp.cp_policy_init(seed)
+    assert w.dtype == np.uint16 and w.shape == (cp.CP_POLICY_WEIGHTS,)
+    assert np.array_equal(w, synth.policy_weights(seed))
+
+
+def test_policy_init_distribution():
+    import numpy as np
+
+    def as_f32(bits):
+        return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+    ws = np.stack([as_f32(cp.cp_policy_init(s)) for s in range(40)])
+    for lo, hi, fan_in in ((0, 256, 4), (256, 4352, 64), (4352, 4480, 64)):
+        v = ws[:, lo:hi].ravel()
+        m = len(v)
+        assert abs(v.mean()) < 4 * np.sqrt(1 / fan_in / m)
+        assert abs(v.var() * fan_in - 1) < 4 * np.sqrt(2 / m)
+        # N(0, 1): a fraction 0.6827 within one standard deviation
+        inside = np.mean(np.abs(v) * np.sqrt(fan_in) < 1)
+        assert abs(inside - 0.6827) < 4 * np.sqrt(0.6827 * 0.3173 / m)
+    assert not np.array_equal(cp.cp_policy_init(0), cp.cp_policy_init(1))
+    assert np.array_equal(cp.cp_policy_init(3), cp.cp_policy_init(3))
+
+
+def test_policy_init_null():
+    assert cp.lib().cp_policy_init(None, 0) == cp.CP_ERR_NULL
+    assert "NULL" in cp.lib().cp_last_error().decode()

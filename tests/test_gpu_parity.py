@@ -204,6 +204,61 @@ def test_rollout_65536x1000_one_step_per_launch(gpu, variant):
         assert np.array_equal(u32(getattr(tr, f))[match], out[f][match]), f
 
 
+def test_graph_replayed_rollouts_match_oracle(gpu):
+    # The launch-bound workload as the benchmark runs it: repeated 1,000-step
+    # rollouts of 65,536 environments on one handle.  The first call of a
+    # kind is launched step by step (and recorded), the second builds the
+    # HIP graph and replays it, the third replays it again (k_words +
+    # k_fused_step_words nodes).  The replayed calls continue the oracle's
+    # rollout from step 1,000 and 2,000.
+    n, T = 65536, 1000
+    s = cp.CartPoleStates(n, variant=cp.CP_FUSED, graphs=True)
+    cp.cp_init(s, 0)
+    # the same outputs every call: a graph is kept per (arrays, outputs, length)
+    tr = cp.Trajectory(n, T, obs=False, reward=False)
+    cp.cp_rollout(s, T, 0, tr)
+    o = O.OracleState(n)
+    O.init(o, 0)
+    O.rollout(o, T)
+    for call in range(2):
+        before = cp.cp_graph_replays()
+        tr.totals.zero_()  # the totals add up across calls
+        cp.cp_rollout(s, T, 0, tr)
+        torch.cuda.synchronize()
+        assert cp.cp_graph_replays() == before + 1, "the call was not replayed"
+        out = O.rollout(o, T, traj=("done",))
+        g, gk, gl = gpu_state(s)
+        match = assert_rollout_match(tr.done.cpu().numpy(), out["done"], g, o.state())
+        for f in ("done_count", "ret_sum"):
+            assert np.array_equal(u32(getattr(tr, f))[match], out[f][match]), f
+        assert np.array_equal(gk[match], o.ep_index[match])
+        assert np.array_equal(gl[match], o.ep_len[match])
+        assert np.all(tr.total_reward.cpu().numpy() == T)
+        tot = tr.totals.cpu().numpy()
+        assert tot[0] == u32(tr.done_count).sum() and tot[1] == u32(tr.ret_sum).sum()
+
+
+@pytest.mark.parametrize("k", [1, 10, 1000])
+def test_unroll_ladder_matches_oracle(gpu, k):
+    # The resident kernel at k steps per launch (the state through HBM every
+    # k steps; the paper's scan unroll factor) on the launch-bound workload,
+    # against the oracle's 65,536 x 1,000 rollout.
+    n, T = 65536, 1000
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, steps_per_launch=k)
+    cp.cp_init(s, 0)
+    tr = cp.Trajectory(n, T, obs=False, reward=False)
+    cp.cp_rollout(s, T, 0, tr)
+    torch.cuda.synchronize()
+    o, out = _oracle_65536x1000()
+    g, gk, gl = gpu_state(s)
+    match = assert_rollout_match(tr.done.cpu().numpy(), out["done"], g, o.state())
+    for f in ("done_count", "ret_sum"):
+        assert np.array_equal(u32(getattr(tr, f))[match], out[f][match]), f
+    assert np.array_equal(gk[match], o.ep_index[match]) and np.array_equal(gl[match], o.ep_len[match])
+    tot = tr.totals.cpu().numpy()
+    assert tot[0] == u32(tr.done_count).sum() and tot[1] == u32(tr.ret_sum).sum()
+
+
 def _sample_ids(n, k, seed):
     rng = np.random.default_rng(seed)
     ids = np.unique(np.concatenate([rng.choice(n, k, replace=False), [0, n - 1]]))

@@ -6,13 +6,13 @@ import ctypes
 import pytest
 import torch
 
-from paper_2301_13062_amd import build as B
+from bench_ref import build as R
 
 pytestmark = pytest.mark.gpu
 
 
 def ref():
-    r = ctypes.CDLL(B.REF_LIB)
+    r = ctypes.CDLL(R.LIB)
     r.cpref_empty.argtypes = [ctypes.c_int, ctypes.c_void_p]
     r.cpref_touch.argtypes = [ctypes.c_void_p] * 8 + [ctypes.c_int64, ctypes.c_void_p]
     return r
