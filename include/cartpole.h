@@ -22,7 +22,8 @@
  *    caller; the library never allocates, frees or retains the caller's
  *    memory and calls no allocator itself.  The one thing it keeps is the
  *    cache of instantiated HIP graphs of cp_rollout (below): runtime objects,
- *    whose kernel-argument storage the HIP runtime provides.
+ *    whose kernel-argument storage the HIP runtime provides, and one event
+ *    per graph.
  *  - Calls are asynchronous on s->stream (a hipStream_t; NULL = the null
  *    stream).  Results are visible after the caller synchronises it.
  *  - Return value: CP_OK (0) or a negative CP_ERR_* code; cp_last_error()
@@ -190,9 +191,11 @@ int cp_step_group(cp_states *const *states, const cp_step_io *io, int32_t count)
  * CP_FUSED with a workspace, below 2^21 environments, 16 to 8192 steps and
  * outside stream capture: a call whose arrays, outputs, workspace and
  * n_steps repeat those of an earlier call is replayed from one HIP graph
- * that the library builds on that second call and keeps (at most 32 per
- * process, for the life of the process); the first call of a kind launches
- * step by step.  Results are the same either way.                          */
+ * that the library builds on that second call and keeps; the first call of
+ * a kind launches step by step.  At most 32 graphs are kept per process:
+ * a new kind then replaces the least recently replayed one, destroyed after
+ * its last replay has finished.  Results are the same either way.
+ * cp_graph_replays() counts the calls that were replayed.                  */
 int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
 
 /* The MLP policy alone (above; weights as for cp_states.policy_w): for each

@@ -301,18 +301,23 @@ struct RolloutKey {
   }
 };
 
-// Graphs are kept for the life of the process (a replay may still be in
-// flight when a later call looks them up); past kMaxGraphs new kinds of
-// rollout run launch by launch.
+// At most kMaxGraphs graphs are kept.  A new kind of rollout met for the
+// second time while the cache is full replaces the least recently used
+// graph, destroyed only after its last replay has finished (an event
+// recorded behind every replay).  Kinds met once are remembered in a list of
+// kMaxSeen, oldest dropped first.
 constexpr size_t kMaxGraphs = 32, kMaxSeen = 64;
 
 struct RolloutGraph {
   RolloutKey key;
   hipGraphExec_t exec;
+  hipEvent_t done;    // recorded on the stream after each replay
+  uint64_t last_use;  // g_clock at the last replay
 };
 
 std::mutex g_graph_mutex;
 std::atomic<uint64_t> g_replays{0};
+uint64_t g_clock = 0;
 std::vector<RolloutGraph> g_graphs;
 std::vector<RolloutKey> g_seen;  // kinds met once, oldest first
 
@@ -361,29 +366,54 @@ hipError_t build_rollout_graph(const RolloutKey &k, hipGraphExec_t *out) {
   return e;
 }
 
-// The graph for this kind of rollout: built on its second call (the first
-// is only recorded), or nullptr.
-hipError_t rollout_graph(const RolloutKey &k, hipGraphExec_t *out) {
+// The cached graph of this kind of rollout, built on its second call (the
+// first is only recorded), or nullptr.  Called with g_graph_mutex held.
+hipError_t rollout_graph(const RolloutKey &k, RolloutGraph **out) {
   *out = nullptr;
-  std::lock_guard<std::mutex> lock(g_graph_mutex);
-  for (const RolloutGraph &rg : g_graphs)
+  for (RolloutGraph &rg : g_graphs)
     if (rg.key == k) {
-      *out = rg.exec;
+      *out = &rg;
       return hipSuccess;
     }
-  if (g_graphs.size() >= kMaxGraphs) return hipSuccess;
-  bool seen = false;
-  for (const RolloutKey &s : g_seen) seen = seen || s == k;
-  if (!seen) {
+  size_t seen = g_seen.size();
+  for (size_t j = 0; j < g_seen.size(); ++j)
+    if (g_seen[j] == k) seen = j;
+  if (seen == g_seen.size()) {
     if (g_seen.size() >= kMaxSeen) g_seen.erase(g_seen.begin());
     g_seen.push_back(k);
     return hipSuccess;
   }
   hipGraphExec_t exec = nullptr;
-  const hipError_t e = build_rollout_graph(k, &exec);
+  hipError_t e = build_rollout_graph(k, &exec);
   if (e != hipSuccess) return e;
-  g_graphs.push_back(RolloutGraph{k, exec});
-  *out = exec;
+  hipEvent_t done = nullptr;
+  e = hipEventCreateWithFlags(&done, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    (void)hipGraphExecDestroy(exec);
+    return e;
+  }
+  g_seen.erase(g_seen.begin() + long(seen));
+  RolloutGraph fresh{k, exec, done, 0};
+  if (g_graphs.size() < kMaxGraphs) {
+    g_graphs.push_back(fresh);
+    *out = &g_graphs.back();
+    return hipSuccess;
+  }
+  size_t lru = 0;
+  for (size_t j = 1; j < g_graphs.size(); ++j)
+    if (g_graphs[j].last_use < g_graphs[lru].last_use) lru = j;
+  RolloutGraph &old = g_graphs[lru];
+  // the evicted graph's last replay must be over before it is destroyed
+  e = hipEventSynchronize(old.done);
+  if (e != hipSuccess) {
+    (void)hipGraphExecDestroy(exec);
+    (void)hipEventDestroy(done);
+    return e;
+  }
+  (void)hipGraphExecDestroy(old.exec);
+  (void)hipEventDestroy(old.done);
+  old = fresh;
+  *out = &old;
   return hipSuccess;
 }
 
@@ -488,17 +518,22 @@ hipError_t launch_fused_graph(const StepParams &base, uint32_t T, void *workspac
   if (e != hipSuccess) return e;
   if (stream != nullptr && hipGetStreamDeviceId(stream) != device) return hipSuccess;
   RolloutKey key{device, base, T, workspace};
-  hipGraphExec_t exec = nullptr;
-  e = rollout_graph(key, &exec);
-  if (e != hipSuccess || !exec) return e;
+  // looked up, launched and marked under the lock, so that no other thread
+  // evicts the graph in between
+  std::lock_guard<std::mutex> lock(g_graph_mutex);
+  RolloutGraph *rg = nullptr;
+  e = rollout_graph(key, &rg);
+  if (e != hipSuccess || !rg) return e;
   hipLaunchKernelGGL(k_graph_set, dim3(1), dim3(64), 0, stream, GraphDesc{base.kact, base.t},
                      static_cast<GraphDesc *>(workspace));
   e = hipGetLastError();
   if (e != hipSuccess) return e;
-  e = hipGraphLaunch(exec, stream);
-  *used = e == hipSuccess;
-  if (*used) g_replays.fetch_add(1u, std::memory_order_relaxed);
-  return e;
+  e = hipGraphLaunch(rg->exec, stream);
+  if (e != hipSuccess) return e;
+  *used = true;
+  rg->last_use = ++g_clock;
+  g_replays.fetch_add(1u, std::memory_order_relaxed);
+  return hipEventRecord(rg->done, stream);
 }
 
 uint64_t graph_replays() { return g_replays.load(std::memory_order_relaxed); }

@@ -115,18 +115,34 @@ def test_rollout_inside_caller_stream_capture(gpu):
 
 
 def test_more_kinds_than_the_graph_cache_holds(gpu):
-    # 40 kinds of rollout (one length each), each called three times: past
-    # the cache's 32 graphs the library launches step by step; results equal
-    # the direct launches throughout (seen-list eviction included)
+    # 40 kinds of rollout (one length each, outputs allocated once), each
+    # called three times.  The cache keeps 32 graphs, replacing the least
+    # recently used: the first round records, the second builds and replays
+    # all 40 (kinds 48..55 displacing 16..23), the third replays the 32 kept
+    # and records 16..23 afresh.  Results equal the direct launches throughout.
     n = 300
     a, b = twins(n, seed=13)
+    kinds = {T: (cp.Trajectory(n, T, stats=False), cp.Trajectory(n, T, stats=False))
+             for T in range(16, 56)}
+    replays = []
     for rep in range(3):
-        for T in range(16, 56):
-            ta, tb = cp.Trajectory(n, T, stats=False), cp.Trajectory(n, T, stats=False)
+        before = cp.cp_graph_replays()
+        for T, (ta, tb) in kinds.items():
             cp.cp_rollout(a, T, T, ta)
             cp.cp_rollout(b, T, T, tb)
             torch.cuda.synchronize()
             assert_same(a, b, ta, tb)
+        replays.append(cp.cp_graph_replays() - before)
+    assert replays == [0, 40, 32]
+    # a kind displaced from the cache replays again from its second call on
+    ta, tb = kinds[16]
+    before = cp.cp_graph_replays()
+    for rep in range(2):
+        cp.cp_rollout(a, 16, 99, ta)
+        cp.cp_rollout(b, 16, 99, tb)
+    torch.cuda.synchronize()
+    assert_same(a, b, ta, tb)
+    assert cp.cp_graph_replays() - before == 2
 
 
 def test_two_threads_replay_concurrently(gpu):
