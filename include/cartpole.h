@@ -198,6 +198,25 @@ int cp_step_group(cp_states *const *states, const cp_step_io *io, int32_t count)
  * cp_graph_replays() counts the calls that were replayed.                  */
 int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
 
+/* For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc: cp_rollout
+ * with nothing allocated by the call and no workspace from the caller.  The
+ * temporaries of CP_UNFUSED and CP_CONCAT live in the library's own scratch,
+ * one array of CP_SCRATCH_BYTES per device, reserved when the library is
+ * loaded on that device and held until the process ends (s->workspace is
+ * ignored); a batch whose temporaries need more (cp_workspace_bytes(n,
+ * variant) > CP_SCRATCH_BYTES: CP_UNFUSED above 222,208 environments,
+ * CP_CONCAT above 2,097,152) is CP_ERR_SIZE, checked before any HIP call.
+ * CP_FUSED launches one kernel per step and never builds or replays a HIP
+ * graph; CP_RESIDENT is cp_rollout.  Results equal cp_rollout's bit for
+ * bit.  Every call on one device shares that device's scratch: calls whose
+ * work overlaps in time on one GPU (other streams, other threads) race and
+ * must not be issued; calls queued one after the other on one stream are
+ * safe.  Nothing in the scratch needs to start cleared (every temporary is
+ * written before it is read within its step).                             */
+#define CP_SCRATCH_BYTES ((size_t)32 << 20)
+int cp_rollout_noalloc(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj);
+
 /* The MLP policy alone (above; weights as for cp_states.policy_w): for each
  * of n environments, actions[i] = 1 (push right) or 0 for the state
  * obs[0..3][i] (x, x_dot, theta, theta_dot planes of n binary32 values, as

@@ -73,6 +73,9 @@ def lib():
         L.cp_init.argtypes = [P(cp_states), ctypes.c_uint64]
         L.cp_step.argtypes = [P(cp_states), _p, _p, _p, _p]
         L.cp_rollout.argtypes = [P(cp_states), ctypes.c_int64, ctypes.c_uint64, P(cp_traj)]
+        L.cp_rollout_noalloc.argtypes = [P(cp_states), ctypes.c_int64, ctypes.c_uint64,
+                                         P(cp_traj)]
+        L.cp_rollout_noalloc.restype = ctypes.c_int
         L.cp_step_group.argtypes = [P(P(cp_states)), P(cp_step_io), ctypes.c_int32]
         L.cp_step_group.restype = ctypes.c_int
         L.cp_policy.argtypes = [_p, ctypes.c_int64, _p, _p, _p]
@@ -204,6 +207,21 @@ def cp_rollout(states: CartPoleStates, n_steps: int, seed: int, traj: Trajectory
     _check(lib().cp_rollout(ctypes.byref(h), int(n_steps), int(seed),
                             ctypes.byref(th) if th is not None else None))
     states._sync_back(h)
+
+
+def cp_rollout_noalloc(states: CartPoleStates, n_steps: int, seed: int,
+                       traj: Trajectory = None) -> None:
+    """cp_rollout without a workspace and without any allocation: the unfused
+    and concatenated levels' temporaries in the library's per-device scratch
+    (cartpole.h)."""
+    h = states.handle()
+    th = traj.handle() if traj is not None else None
+    _check(lib().cp_rollout_noalloc(ctypes.byref(h), int(n_steps), int(seed),
+                                    ctypes.byref(th) if th is not None else None))
+    states._sync_back(h)
+
+
+CP_SCRATCH_BYTES = 32 << 20
 
 
 def cp_policy(obs, policy_w, actions, stream=None) -> None:

@@ -9,7 +9,7 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(OUT_DIR, "libcartpole.so")
 
-SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip"]
+SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip", "cp_scratch.hip"]
 # A plain C client of the ABI (cartpole.h and the HIP runtime API only), built
 # with the host C compiler; the GPU tests run it.
 CLIENT_SRC = os.path.join(ROOT, "tests", "capi_client.c")

@@ -97,10 +97,12 @@ int check_workspace(const cp_states *s) {
   return CP_OK;
 }
 
-// One step of the per-step levels (unfused, concatenated, fused).
-hipError_t launch_step(const cp_states *s, const cp::StepParams &p, hipStream_t st) {
-  if (s->variant == CP_UNFUSED) return cp::launch_unfused_step(p, s->workspace, st);
-  if (s->variant == CP_CONCAT) return cp::launch_concat_step(p, s->workspace, st);
+// One step of the per-step levels (unfused, concatenated, fused); the
+// temporaries of the first two in `workspace`.
+hipError_t launch_step(const cp_states *s, const cp::StepParams &p, void *workspace,
+                       hipStream_t st) {
+  if (s->variant == CP_UNFUSED) return cp::launch_unfused_step(p, workspace, st);
+  if (s->variant == CP_CONCAT) return cp::launch_concat_step(p, workspace, st);
   return cp::launch_fused_step(p, st);
 }
 
@@ -235,7 +237,7 @@ CP_API int cp_step(cp_states *s, const uint8_t *actions, float *obs, float *rewa
     p.reward = reward;
     p.done = done;
     // Explicit actions under CP_RESIDENT: a single step is the fused step.
-    err = launch_step(s, p, st);
+    err = launch_step(s, p, s->workspace, st);
   }
   if (int e = hip_status(err, "cp_step launch")) return e;
   s->t += 1;
@@ -307,13 +309,14 @@ CP_API int cp_step_group(cp_states *const *states, const cp_step_io *io, int32_t
   return ok();
 }
 
-CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj) {
+namespace {
+
+// Everything cp_rollout checks except the workspace (which the entry point
+// that allocates nothing replaces by the library's scratch).
+int check_rollout(const cp_states *s, int64_t n_steps, const cp_traj &tr) {
   if (int e = check_states(s)) return e;
   if (n_steps < 0) return fail(CP_ERR_SIZE, "n_steps = %lld is negative", (long long)n_steps);
   if (int e = check_steps(s, uint64_t(n_steps))) return e;
-  if (int e = check_workspace(s)) return e;
-  cp_traj none{};
-  const cp_traj &tr = traj ? *traj : none;
   if ((tr.obs && !aligned_to(tr.obs, elem_bytes(s->precision))) ||
       (tr.reward && !aligned4(tr.reward)) ||
       (tr.done_count && !aligned4(tr.done_count)) ||
@@ -339,6 +342,13 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
   if (int e = check_precision_step(s, false)) return e;
   if (s->steps_per_launch < 0)
     return fail(CP_ERR_SIZE, "steps_per_launch = %lld is negative", (long long)s->steps_per_launch);
+  return CP_OK;
+}
+
+// The rollout itself, after validation; `workspace` stands in for
+// s->workspace, and graphs = false never builds or replays a HIP graph.
+int run_rollout(cp_states *s, int64_t n_steps, uint64_t seed, const cp_traj &tr,
+                void *workspace, bool graphs) {
   if (n_steps == 0) return ok();
 
   hipStream_t st = static_cast<hipStream_t>(s->stream);
@@ -390,13 +400,13 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
     // With a CP_FUSED workspace, a rollout that repeats an earlier call's
     // arrays, outputs and length is replayed from a HIP graph.
     bool replayed = false;
-    if (s->variant == CP_FUSED && s->workspace && !obs_state &&
+    if (graphs && s->variant == CP_FUSED && workspace && !obs_state &&
         n_steps <= int64_t(cp::kGraphMaxSteps)) {
       p.t = uint32_t(s->t);
       p.obs = tr.obs;
       p.reward = tr.reward;
       p.done = tr.done;
-      if (int e = hip_status(cp::launch_fused_graph(p, uint32_t(n_steps), s->workspace, st,
+      if (int e = hip_status(cp::launch_fused_graph(p, uint32_t(n_steps), workspace, st,
                                                     &replayed),
                              "cp_rollout graph"))
         return e;
@@ -421,7 +431,7 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
         p.th = last ? s->theta : nullptr;
         p.thd = last ? s->theta_dot : nullptr;
       }
-      const hipError_t err = launch_step(s, p, st);
+      const hipError_t err = launch_step(s, p, workspace, st);
       if (int e = hip_status(err, "cp_rollout launch")) {
         s->t += uint64_t(j);  // steps already queued stay counted
         return e;
@@ -438,6 +448,35 @@ CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *tra
   }
   s->t += uint64_t(n_steps);
   return ok();
+}
+
+}  // namespace
+
+CP_API int cp_rollout(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj) {
+  cp_traj none{};
+  const cp_traj &tr = traj ? *traj : none;
+  if (int e = check_rollout(s, n_steps, tr)) return e;
+  if (int e = check_workspace(s)) return e;
+  return run_rollout(s, n_steps, seed, tr, s->workspace, true);
+}
+
+CP_API int cp_rollout_noalloc(cp_states *s, int64_t n_steps, uint64_t seed, cp_traj *traj) {
+  cp_traj none{};
+  const cp_traj &tr = traj ? *traj : none;
+  if (int e = check_rollout(s, n_steps, tr)) return e;
+  void *scratch = nullptr;
+  if (s->variant == CP_UNFUSED || s->variant == CP_CONCAT) {
+    const size_t need = workspace_need(s->variant, uint32_t(s->n));
+    if (need > CP_SCRATCH_BYTES)
+      return fail(CP_ERR_SIZE, "%s needs %zu bytes of temporaries for n = %lld; the scratch "
+                  "holds %zu", s->variant == CP_UNFUSED ? "CP_UNFUSED" : "CP_CONCAT", need,
+                  (long long)s->n, size_t(CP_SCRATCH_BYTES));
+    static_assert(CP_SCRATCH_BYTES == cp::kScratchBytes, "scratch size");
+    if (n_steps == 0) return ok();
+    if (int e = hip_status(cp::scratch_address(&scratch), "cp_rollout_noalloc scratch"))
+      return e;
+  }
+  return run_rollout(s, n_steps, seed, tr, scratch, false);
 }
 
 CP_API int cp_policy(const float *obs, int64_t n, const uint16_t *policy_w, uint8_t *actions,

@@ -122,6 +122,12 @@ hipError_t launch_group_step(GroupParams g, hipStream_t stream);
 size_t concat_workspace_bytes(uint32_t n);
 hipError_t launch_concat_step(const StepParams &p, void *workspace, hipStream_t stream);
 
+// The library's per-device scratch (cp_scratch.hip) for the entry point that
+// allocates nothing: kScratchBytes, 256-byte aligned; its device address on
+// the current device (looked up once per device).
+constexpr size_t kScratchBytes = size_t(32) << 20;
+hipError_t scratch_address(void **out);
+
 // Unfused level: one kernel per primitive operation; temporaries live in the
 // caller's workspace.
 size_t unfused_workspace_bytes(uint32_t n);

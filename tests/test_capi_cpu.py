@@ -404,3 +404,31 @@ def test_policy_init_distribution():
 def test_policy_init_null():
     assert cp.lib().cp_policy_init(None, 0) == cp.CP_ERR_NULL
     assert "NULL" in cp.lib().cp_last_error().decode()
+
+
+# --------------------------------------------------------------------------- no allocation
+def test_noalloc_validates_before_any_hip_call():
+    L = cp.lib()
+    L.cp_rollout_noalloc.argtypes = [ctypes.POINTER(cp.cp_states), ctypes.c_int64,
+                                     ctypes.c_uint64, ctypes.POINTER(cp.cp_traj)]
+    assert L.cp_rollout_noalloc(None, 1, 0, None) == cp.CP_ERR_NULL
+    # the scratch holds the temporaries of at most 222,208 unfused and
+    # 2,097,152 concatenated environments
+    assert cp.cp_workspace_bytes(222208, cp.CP_UNFUSED) <= cp.CP_SCRATCH_BYTES
+    assert cp.cp_workspace_bytes(222209, cp.CP_UNFUSED) > cp.CP_SCRATCH_BYTES
+    assert cp.cp_workspace_bytes(1 << 21, cp.CP_CONCAT) <= cp.CP_SCRATCH_BYTES
+    far = 1 << 36
+    for variant, n in ((cp.CP_UNFUSED, 222209), (cp.CP_CONCAT, (1 << 21) + 1)):
+        h = handle(variant=variant, n=n, x=A, x_dot=A + far, theta=A + 2 * far,
+                   theta_dot=A + 3 * far, ep_index=A + 4 * far, ep_len=A + 5 * far)
+        assert L.cp_rollout_noalloc(ctypes.byref(h), 2, 0, None) == cp.CP_ERR_SIZE
+        assert "scratch" in cp.lib().cp_last_error().decode() and h.t == 7
+    # the same checks as cp_rollout come first; no workspace is needed
+    h = handle(variant=cp.CP_UNFUSED)
+    assert L.cp_rollout_noalloc(ctypes.byref(h), -1, 0, None) == cp.CP_ERR_SIZE
+    assert L.cp_rollout_noalloc(ctypes.byref(h), 0, 0, None) == cp.CP_OK  # no-op
+    tr = cp.cp_traj(A, None, None, None, None, None, None)  # obs over the state
+    assert L.cp_rollout_noalloc(ctypes.byref(h), 2, 0, ctypes.byref(tr)) == cp.CP_ERR_OVERLAP
+    h = handle(variant=cp.CP_FUSED, policy_w=A + 0x900000)
+    assert L.cp_rollout_noalloc(ctypes.byref(h), 2, 0, None) == cp.CP_ERR_UNSUPPORTED
+    assert h.t == 7
