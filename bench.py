@@ -60,14 +60,25 @@ METRIC = "env-steps/sec on 1 MI355X; achieved HBM GB/s (or VALU %) vs peak"
 # Algorithmic HBM bytes per environment-step of the fused step kernel in a
 # rollout that writes the trajectory.  Small batches (65,536): reads x,
 # x_dot, theta, theta_dot, ep_len (20 B); writes them (20 B) plus obs (16 B),
-# reward (4 B) and done (1 B).  Large batches (from 2^21 environments) read
-# the state from the previous step's obs plane and write it only there:
-# reads 20 B, writes obs, ep_len, reward, done (25 B); the first step reads,
-# and the last writes, the state arrays (16 B once per rollout).  The
-# episode index is read and written only on termination (about 4.5% of
-# steps) and is not counted.
+# reward (4 B) and done (1 B); the episode index (touched at terminations)
+# is not counted.  Large batches (from 2^21 environments, the streaming
+# rollout): every step reads the previous step's obs plane (16 B) and writes
+# obs, reward and done (21 B); a terminating environment also reads and
+# writes its episode index and writes its episode length (12 B); once per
+# rollout the first step reads both counters and parks them in the state
+# arrays (16 B) and the last step reads counters and parked values and
+# writes state and counters (40 B).
 STEP_BYTES_WITH_OUTPUTS = 61
-STEP_BYTES_TRAJ_LARGE = 45
+STEP_BYTES_STREAM = 16 + 21
+STEP_BYTES_STREAM_TERMINATION = 12
+ROLLOUT_BYTES_STREAM = 16 + 40
+
+
+def stream_bytes_per_env_step(termination_rate, T):
+    """Algorithmic bytes per environment-step of a streaming rollout of T
+    steps whose environment-steps terminate at the given rate."""
+    return STEP_BYTES_STREAM + STEP_BYTES_STREAM_TERMINATION * termination_rate + \
+        ROLLOUT_BYTES_STREAM / T
 # The whole-rollout kernel writing the same trajectory keeps the state in
 # registers: obs 16, reward 4, done 1 written per env-step, nothing read.
 STEP_BYTES_TRAJ_RESIDENT = 21
@@ -239,9 +250,11 @@ def bench_streaming(cp, K, W):
     for _ in range(max(W, 1)):
         cp.cp_rollout(s, T, 0, tr)
     wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=K)
+    # terminations of the last rollout (the rate the algorithmic bytes need)
+    rate = tr.done.sum(dtype=torch.int64).item() / (n * T)
     out = {"envs": n, "steps_per_rollout": T, "rollouts": K, "wall_ms": wall, "event_ms": ev,
            "env_steps_per_s": n * T * K / (wall * 1e-3), "ms_per_rollout": wall / K,
-           "kernel_mean_us": ev * 1e3 / (K * T)}
+           "kernel_mean_us": ev * 1e3 / (K * T), "termination_rate": rate}
     del s, tr
     torch.cuda.empty_cache()
     return out
@@ -358,7 +371,8 @@ def bench_fill():
 
 
 VALU_REFERENCE_FORMS = ("fma_f32_vgpr", "fma_f32_sgpr_operand", "rotate_u32", "rcp_f32", "fma_f64",
-                        "rcp_f64", "pk_fma_f16", "fma_f16", "mul_f16")
+                        "rcp_f64", "pk_fma_f16", "fma_f16", "mul_f16", "pk_mul_f16", "pk_add_f16",
+                        "fma_mixlo_f16")
 
 
 def bench_valu_reference():
@@ -816,7 +830,8 @@ def cpu_baseline(stride=32, chunk=1 << 16):
 def headline_line(head, K, W):
     n, T = head["envs"], head["steps_per_rollout"]
     kern_us = head["kernel_mean_us"]
-    gbs = STEP_BYTES_TRAJ_LARGE * n / (kern_us * 1e-6) / 1e9
+    bpe = stream_bytes_per_env_step(head["termination_rate"], T)
+    gbs = bpe * n / (kern_us * 1e-6) / 1e9
     c = COUNTERS["fused_step_16777216"]
     return {
         "metric": METRIC,
@@ -840,8 +855,9 @@ def headline_line(head, K, W):
                      "frac": gbs / HBM_PEAK_GBS,
                      "traffic": measured_traffic_bytes("fused_step_16777216"),
                      "traffic_stored_counters": True, "traffic_profile": c["profile"],
-                     "bytes_per_env_step": STEP_BYTES_TRAJ_LARGE,
-                     "kernel": "k_fused_step<false, false, true, true>",
+                     "bytes_per_env_step": bpe,
+                     "termination_rate": head["termination_rate"],
+                     "kernel": "k_stream_step (kFirst, kMid x 98, kLast)",
                      "kernel_mean_us": kern_us, "launches_timed": K * T},
     }
 

@@ -16,6 +16,9 @@
 //   6  packed binary16 FMA, two values per lane (v_pk_fma_f16)
 //   7  binary16 FMA, one value per lane (v_fma_f16)
 //   8  binary16 multiply, one value per lane (v_mul_f16)
+//   9  packed binary16 multiply, two values per lane (v_pk_mul_f16)
+//  10  packed binary16 add, two values per lane (v_pk_add_f16)
+//  11  mixed-precision multiply-add rounded once to binary16 (v_fma_mixlo_f16)
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -80,6 +83,10 @@ __global__ __launch_bounds__(kBlock) void k_chains(float *__restrict__ out, floa
         // chains into packed instructions)
         if (kForm == 7) asm volatile("v_fma_f16 %0, %0, %1, %2" : "+v"(hs[i]) : "v"(sb), "v"(sc));
         if (kForm == 8) asm volatile("v_mul_f16_e32 %0, %1, %0" : "+v"(hs[i]) : "v"(sb));
+        if (kForm == 9) h[i] = h[i] * hb;
+        if (kForm == 10) h[i] = h[i] + hc;
+        if (kForm == 11)
+          asm volatile("v_fma_mixlo_f16 %0, %0, %1, 0 op_sel_hi:[1,0,0]" : "+v"(hs[i]) : "v"(vb));
       }
     }
   }
@@ -93,7 +100,7 @@ __global__ __launch_bounds__(kBlock) void k_chains(float *__restrict__ out, floa
 
 }  // namespace
 
-// Launches `blocks` blocks of 256 lanes of form `form` (0..8 above), each
+// Launches `blocks` blocks of 256 lanes of form `form` (0..11 above), each
 // lane issuing iters * cpref_ops_per_iter() instructions; out must hold
 // blocks * 256 floats (device memory).  Returns 0, or -1 for a bad argument
 // or a launch failure.
@@ -113,6 +120,9 @@ extern "C" __attribute__((visibility("default"))) int cpref_chains(int form, int
     case 6: hipLaunchKernelGGL(k_chains<6>, grid, block, 0, s, out, 0.9999f, 0.5f, iters); break;
     case 7: hipLaunchKernelGGL(k_chains<7>, grid, block, 0, s, out, 0.9999f, 0.5f, iters); break;
     case 8: hipLaunchKernelGGL(k_chains<8>, grid, block, 0, s, out, 0.9999f, 0.5f, iters); break;
+    case 9: hipLaunchKernelGGL(k_chains<9>, grid, block, 0, s, out, 0.9999f, 0.5f, iters); break;
+    case 10: hipLaunchKernelGGL(k_chains<10>, grid, block, 0, s, out, 0.9999f, 0.5f, iters); break;
+    case 11: hipLaunchKernelGGL(k_chains<11>, grid, block, 0, s, out, 0.9999f, 0.5f, iters); break;
     default: return -1;
   }
   return hipGetLastError() == hipSuccess ? 0 : -1;

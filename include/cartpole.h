@@ -30,7 +30,7 @@
  *    then gives a message (per calling thread).  Arguments are validated
  *    before any HIP call: on CP_ERR_NULL/SIZE/ALIGN/RANGE/UNSUPPORTED/OVERLAP
  *    nothing is launched and *s is unchanged.  CP_ERR_HIP reports a failed
- *    launch.
+ *    launch; the handle's arrays then hold unspecified values.
  *  - Outputs must not overlap the state arrays or each other: cp_step and
  *    cp_rollout compare the byte ranges of every output they are given with
  *    those of the state arrays and of the other outputs, and return
@@ -132,7 +132,11 @@ typedef struct cp_states {
  * environment, over this rollout: done_count, total_reward (the sum of the
  * rewards), ret_sum (sum of the returns of the episodes that ended in it).
  * global[0] += total terminations, global[1] += sum of those returns (the
- * caller clears global before the first call it wants counted).  obs holds
+ * caller clears global before the first call it wants counted).  Exact for
+ * CP_RESIDENT and for CP_FUSED from 2^21 environments with an obs
+ * trajectory; the per-step levels otherwise take them from the growth of
+ * the summed episode indices and lengths, exact unless an environment's
+ * episode index or length passes 2^32 - 1 within the call.  obs holds
  * values of the handle's precision (double / _Float16 cast to float *).    */
 typedef struct cp_traj {
     float *obs;

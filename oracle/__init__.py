@@ -332,7 +332,8 @@ def rollout_prec(st: OracleStateP, T, act_seed=None, actions=None, traj=False):
                             _ptr(out["total_reward"], np.float32), _ptr(out["ret_sum"], np.uint32))
     for f, a in zip(("x", "x_dot", "theta", "theta_dot"), s):
         converted = a.astype(st.dtype)
-        assert np.array_equal(converted.astype(np.float64), a)  # values of the precision
+        # values of the precision (a NaN state stays NaN)
+        assert np.array_equal(converted.astype(np.float64), a, equal_nan=True)
         setattr(st, f, converted)
     if obs is not None:
         out["obs"] = obs.astype(st.dtype)

@@ -9,7 +9,8 @@ INCLUDE = os.path.join(ROOT, "include")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(OUT_DIR, "libcartpole.so")
 
-SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip", "cp_scratch.hip"]
+SOURCES = ["cp_capi.hip", "cp_step.hip", "cp_unfused.hip", "cp_policy.hip", "cp_scratch.hip",
+           "cp_resident16.hip"]
 # A plain C client of the ABI (cartpole.h and the HIP runtime API only), built
 # with the host C compiler; the GPU tests run it.
 CLIENT_SRC = os.path.join(ROOT, "tests", "capi_client.c")
@@ -27,6 +28,8 @@ FLAGS = [
     # consumes them reads them, instead of accumulation registers copied out
     # one value at a time (3% faster MLP rollouts, same results)
     "-mllvm", "-amdgpu-mfma-vgpr-form=1",
+    # room for the compile-time binary16 sin/cos table (cp_f16_table.h)
+    "-fconstexpr-steps=20000000",
     "-Wall",
 ]
 

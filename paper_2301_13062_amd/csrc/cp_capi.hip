@@ -385,18 +385,24 @@ int run_rollout(cp_states *s, int64_t n_steps, uint64_t seed, const cp_traj &tr,
     p.done_count = tr.done_count;
     p.total_reward = tr.total_reward;
     p.ret_sum = tr.ret_sum;
-    if (tr.global)
+    // With an obs trajectory of two steps or more the fused rollout streams:
+    // each step reads its state from the previous step's obs plane, touches
+    // the episode counters only at terminations, and the last step rebuilds
+    // the counters and statistics and writes the state arrays (the
+    // trajectory already holds every intermediate state).  Used for batches
+    // whose state does not stay in the caches between launches (below that
+    // size the state arrays are re-read from cache, while the trajectory is
+    // written past it).
+    const bool obs_state =
+        s->variant == CP_FUSED && tr.obs && n >= cp::kObsStateMinEnvs && n_steps >= 2;
+    // Totals of the per-step levels: the growth of the summed episode
+    // indices and lengths, from one kernel before the steps and one after
+    // (the streaming rollout's last step adds exact ones itself).
+    if (tr.global && !obs_state)
       if (int e = hip_status(cp::launch_episode_sums(s->ep_index, s->ep_len, p.n, false, 0u,
                                                      tr.global, st),
                              "cp_rollout totals"))
         return e;
-    // With an obs trajectory the fused step reads its state from the
-    // previous step's obs plane and writes the state arrays only at the
-    // last step: the trajectory already holds every intermediate state.
-    // Used for batches whose state does not stay in the caches between
-    // launches (below that size the state arrays are re-read from cache,
-    // while the trajectory is written past it).
-    const bool obs_state = s->variant == CP_FUSED && tr.obs && n >= cp::kObsStateMinEnvs;
     // With a CP_FUSED workspace, a rollout that repeats an earlier call's
     // arrays, outputs and length is replayed from a HIP graph.
     bool replayed = false;
@@ -417,6 +423,7 @@ int run_rollout(cp_states *s, int64_t n_steps, uint64_t seed, const cp_traj &tr,
       p.obs = tr.obs ? tr.obs + size_t(j) * 4u * n : nullptr;
       p.reward = tr.reward ? tr.reward + size_t(j) * n : nullptr;
       p.done = tr.done ? tr.done + size_t(j) * n : nullptr;
+      hipError_t err;
       if (obs_state) {
         if (j > 0) {
           const float *prev = tr.obs + size_t(j - 1) * 4u * n;
@@ -425,19 +432,16 @@ int run_rollout(cp_states *s, int64_t n_steps, uint64_t seed, const cp_traj &tr,
           p.thi = prev + 2u * n;
           p.thdi = prev + 3u * n;
         }
-        const bool last = j == n_steps - 1;
-        p.x = last ? s->x : nullptr;
-        p.xd = last ? s->x_dot : nullptr;
-        p.th = last ? s->theta : nullptr;
-        p.thd = last ? s->theta_dot : nullptr;
+        err = cp::launch_stream_step(p, uint32_t(j), uint32_t(n_steps), tr.global, st);
+      } else {
+        err = launch_step(s, p, workspace, st);
       }
-      const hipError_t err = launch_step(s, p, workspace, st);
       if (int e = hip_status(err, "cp_rollout launch")) {
         s->t += uint64_t(j);  // steps already queued stay counted
         return e;
       }
     }
-    if (tr.global)
+    if (tr.global && !obs_state)
       if (int e = hip_status(cp::launch_episode_sums(s->ep_index, s->ep_len, p.n, true,
                                                      uint64_t(n) * uint64_t(n_steps), tr.global,
                                                      st),

@@ -1,0 +1,103 @@
+// cp_f16_table.h -- sin and cos of every binary16 angle in [0, 1/4],
+// each rounded once to binary16 (to nearest, ties to even), as a table
+// computed at compile time: entry b (b = 0 .. 0x3400, the bit patterns of
+// the non-negative binary16 values up to 1/4) holds the bits of RN16(sin x)
+// in its low half and of RN16(cos x) in its high half, x the value of b.
+// The binary16 step looks its sines and cosines up here (an angle a state
+// holds never exceeds the 12-degree limit); sin(-x) = -sin(x), cos(-x) =
+// cos(x).  Usable from host and device code (the host build is what the
+// CPU test prints and compares with the C library's binary64 sin and cos).
+#pragma once
+
+#include <stdint.h>
+
+namespace cp {
+namespace f16tab {
+
+constexpr uint32_t kLast = 0x3400u;  // binary16 1/4
+constexpr uint32_t kEntries = kLast + 1u;
+
+// 2^e for -24 <= e <= 24, by binary exponentiation (exact).
+constexpr double pow2(int e) {
+  double b = e < 0 ? 0.5 : 2.0, v = 1.0;
+  for (unsigned k = unsigned(e < 0 ? -e : e); k; k >>= 1, b *= b)
+    if (k & 1u) v *= b;
+  return v;
+}
+
+// The value of a non-negative binary16 bit pattern (finite).
+constexpr double value_of(uint32_t b) {
+  const uint32_t e = (b >> 10) & 31u, m = b & 1023u;
+  return e == 0u ? double(m) * 0x1p-24 : (1024.0 + double(m)) * pow2(int(e) - 25);
+}
+
+// Taylor polynomials through x^15 / x^14 in binary64: on [0, 1/4] the first
+// omitted terms are below 2^-67 relative, so the sums are within a few
+// binary64 ulp of sin x and cos x -- far inside the distance of any of these
+// values from a binary16 rounding boundary (checked for every entry).
+constexpr double sin_poly(double x) {
+  const double z = x * x;
+  double p = -1.0 / 1307674368000.0;  // -1/15!
+  p = p * z + 1.0 / 6227020800.0;     //  1/13!
+  p = p * z - 1.0 / 39916800.0;       // -1/11!
+  p = p * z + 1.0 / 362880.0;         //  1/9!
+  p = p * z - 1.0 / 5040.0;           // -1/7!
+  p = p * z + 1.0 / 120.0;            //  1/5!
+  p = p * z - 1.0 / 6.0;              // -1/3!
+  return x + (x * z) * p;
+}
+
+constexpr double cos_poly(double x) {
+  const double z = x * x;
+  double q = -1.0 / 87178291200.0;    // -1/14!
+  q = q * z + 1.0 / 479001600.0;      //  1/12!
+  q = q * z - 1.0 / 3628800.0;        // -1/10!
+  q = q * z + 1.0 / 40320.0;          //  1/8!
+  q = q * z - 1.0 / 720.0;            // -1/6!
+  q = q * z + 1.0 / 24.0;             //  1/4!
+  q = q * z - 0.5;                    // -1/2!
+  return 1.0 + z * q;
+}
+
+// t >= 0 rounded to an integer, ties to even.
+constexpr double round_half_even(double t) {
+  const double f = double(static_cast<long long>(t));
+  const double r = t - f;
+  if (r > 0.5) return f + 1.0;
+  if (r < 0.5) return f;
+  return (static_cast<long long>(f) & 1) ? f + 1.0 : f;
+}
+
+// Bits of the binary16 value nearest to v, 0 <= v <= 1 (ties to even):
+// v scaled by its quantum (an exact power-of-two scaling) and rounded.
+constexpr uint32_t nearest_bits(double v) {
+  if (v < 0x1p-14) return uint32_t(round_half_even(v * 0x1p24));  // subnormal quantum 2^-24
+  int e = 0;  // 2^e <= v < 2^(e + 1); v <= 1, so e <= 0
+  double lo = 1.0;
+  while (v < lo) {
+    lo *= 0.5;
+    --e;
+  }
+  double r = round_half_even(v * (1024.0 / lo));  // in [1024, 2048]
+  if (r == 2048.0) {
+    r = 1024.0;
+    ++e;
+  }
+  return (uint32_t(e + 15) << 10) | uint32_t(r - 1024.0);
+}
+
+struct Table {
+  uint32_t v[kEntries];
+};
+
+constexpr Table make_table() {
+  Table t{};
+  for (uint32_t b = 0; b < kEntries; ++b) {
+    const double x = value_of(b);
+    t.v[b] = nearest_bits(sin_poly(x)) | (nearest_bits(cos_poly(x)) << 16);
+  }
+  return t;
+}
+
+}  // namespace f16tab
+}  // namespace cp

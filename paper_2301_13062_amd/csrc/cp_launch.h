@@ -12,8 +12,8 @@ namespace cp {
 
 // Batch state and the per-step outputs of one step (fused or unfused).
 struct StepParams {
-  // state read by the step, and state written (nullptr: not written, when a
-  // trajectory's obs plane already holds it); usually the same arrays
+  // state read by the step (the state arrays, or a streaming rollout's
+  // previous obs plane) and the state arrays written
   const float *xi, *xdi, *thi, *thdi;
   float *x, *xd, *th, *thd;
   uint32_t *ep_index, *ep_len;
@@ -78,6 +78,16 @@ hipError_t launch_init(void *x, void *xd, void *th, void *thd, uint32_t *ep_inde
                        uint32_t *ep_len, uint32_t n, uint32_t env_base, U2 krst, int precision,
                        hipStream_t stream);
 hipError_t launch_fused_step(const StepParams &p, hipStream_t stream);
+// Step j of a streaming fused rollout of T >= 2 steps with random actions
+// and an obs trajectory: p.xi.. the state arrays (j = 0) or the previous
+// step's obs planes, p.x.. the state arrays, p.obs / reward / done the
+// step's rows.  The counters and the per-environment statistics are final
+// only after step T - 1; between the first and the last step the state
+// arrays hold the starting counters (cp_step.hip).  The last step adds the
+// rollout's terminations and finished returns to global[0], global[1]
+// (global may be nullptr).
+hipError_t launch_stream_step(const StepParams &p, uint32_t j, uint32_t T,
+                              unsigned long long *global, hipStream_t stream);
 // A fused rollout of T steps with random actions from one cached HIP graph,
 // for a rollout whose arrays, outputs and length repeat those of an earlier
 // call (base: step 0's parameters, obs/reward/done at row 0; its step
@@ -92,6 +102,11 @@ uint64_t graph_replays();
 // actions (launch_resident_policy), otherwise the random action stream.
 hipError_t launch_resident(const RolloutParams &p, hipStream_t stream);
 hipError_t launch_resident_policy(const RolloutParams &p, hipStream_t stream);
+// The binary16 resident rollout with two environments per lane
+// (cp_resident16.hip), for launches whose first environment is a multiple
+// of 64 (resident_f16x2_applies); the same results as the generic one.
+bool resident_f16x2_applies(const RolloutParams &p);
+hipError_t launch_resident_f16x2(const RolloutParams &p, hipStream_t stream);
 // The MLP policy alone: actions[i] (0/1) for the state obs[0..3][i].
 hipError_t launch_policy_actions(const float *obs, uint32_t n, const uint16_t *policy_w,
                                  uint8_t *actions, hipStream_t stream);

@@ -1,0 +1,331 @@
+// cp_resident16.hip -- the register-resident rollout in binary16 with two
+// environments per lane (the binary16 precision of the hand-written CUDA
+// port the paper compares against, Sec. "Comparison with CUDA
+// implementation"), used when the launch's first environment is a multiple
+// of 64.  Results equal the one-environment-per-lane binary16 kernel bit
+// for bit (every operation the correctly rounded binary16 operation); only
+// the instruction selection differs:
+//  * lane L of a wave holds environments base + L and base + 64 + L in the
+//    low and high halves of packed registers; additions, subtractions and
+//    products of the step are packed binary16 instructions (v_pk_add_f16,
+//    v_pk_mul_f16: two values, each rounded once);
+//  * sin and cos of an angle up to 1/4 are read from a table of the
+//    correctly rounded binary16 values (cp_f16_table.h) staged in LDS, one
+//    ds_read_b32 per environment for both;
+//  * a / m (the binary16 total mass) is one mixed-precision multiply-add
+//    rounding the exact product a * RN32(1/m) once to binary16: equal to the
+//    correctly rounded quotient for every binary16 a, the exact quotients
+//    lying at least 2^-21 (relative) from a binary16 rounding boundary while
+//    RN32(1/m) is within 2^-24 of 1/m;
+//  * the angular acceleration num / den is num times the binary32
+//    reciprocal of den (refined by one Newton step: within 2^-24 (1 + 2^-22)
+//    relative), rounded once the same way: every divisor the step can form
+//    lies in [0.621, 0.667] (94 binary16 values), and for each of them every
+//    binary16 quotient lies at least 2^-22.4 from a rounding boundary.
+// The actions of a wave's 128 environments are two 64-environment blocks of
+// the random stream, each a lane mask (one select per environment).
+#include "cp_f16_table.h"
+#include "cp_launch.h"
+#include "cp_resident.h"
+
+namespace cp {
+
+namespace {
+
+typedef _Float16 h2 __attribute__((ext_vector_type(2)));
+
+constexpr int kBlock16 = 1024;  // 16 waves share one LDS copy of the table
+constexpr int kWaves16 = kBlock16 / 64;
+constexpr uint32_t kEnvsPerWave = 128u;
+
+// The table, evaluated at compile time.
+__device__ const f16tab::Table kSinCos16 = f16tab::make_table();
+
+__device__ __forceinline__ uint32_t bits(h2 v) { return __builtin_bit_cast(uint32_t, v); }
+__device__ __forceinline__ h2 of_bits(uint32_t u) { return __builtin_bit_cast(h2, u); }
+
+// RN16(a * c) for both halves of a (exact product, one rounding; the
+// addend -0 keeps the sign of a zero product).
+__device__ __forceinline__ h2 mul_round2(h2 a, float c) {
+  uint32_t r;
+  asm volatile("v_fma_mixlo_f16 %0, %1, %2, neg(0) op_sel_hi:[1,0,0]"
+               : "=v"(r) : "v"(bits(a)), "v"(c));
+  asm volatile("v_fma_mixhi_f16 %0, %1, %2, neg(0) op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+               : "+v"(r) : "v"(bits(a)), "v"(c));
+  return of_bits(r);
+}
+
+// RN16(a[0] * c0) and RN16(a[1] * c1).
+__device__ __forceinline__ h2 mul_round2(h2 a, float c0, float c1) {
+  uint32_t r;
+  asm volatile("v_fma_mixlo_f16 %0, %1, %2, neg(0) op_sel_hi:[1,0,0]"
+               : "=v"(r) : "v"(bits(a)), "v"(c0));
+  asm volatile("v_fma_mixhi_f16 %0, %1, %2, neg(0) op_sel:[1,0,0] op_sel_hi:[1,0,0]"
+               : "+v"(r) : "v"(bits(a)), "v"(c1));
+  return of_bits(r);
+}
+
+// The binary32 reciprocal of a binary16 divisor, one Newton step after the
+// hardware estimate.
+__device__ __forceinline__ float recip(_Float16 d) {
+  const float b = float(d);
+  const float y0 = __builtin_amdgcn_rcpf(b);
+  const float e = __builtin_fmaf(-b, y0, 1.0f);
+  return __builtin_fmaf(e, y0, y0);
+}
+
+struct S2 {
+  h2 x, xd, th, thd;
+};
+
+// sin and cos of both angles as the one-per-lane kernel computes them, for
+// angles beyond the table (out of line: states the library produces never
+// hold one after their first step).  Returns sin in the low and cos in the
+// high half of each environment's word.
+__device__ __attribute__((noinline)) uint64_t sincos2_beyond(uint32_t t) {
+  half_t s0, c0, s1, c1;
+  sincos16(__builtin_bit_cast(half_t, uint16_t(t)), s0, c0);
+  sincos16(__builtin_bit_cast(half_t, uint16_t(t >> 16)), s1, c1);
+  const uint32_t e0 = uint32_t(__builtin_bit_cast(uint16_t, s0)) |
+                      (uint32_t(__builtin_bit_cast(uint16_t, c0)) << 16);
+  const uint32_t e1 = uint32_t(__builtin_bit_cast(uint16_t, s1)) |
+                      (uint32_t(__builtin_bit_cast(uint16_t, c1)) << 16);
+  return (static_cast<uint64_t>(e1) << 32) | e0;
+}
+
+// sin and cos of both angles of th: from the table when every lane's angles
+// are at most 1/4 in magnitude, else for the whole wave out of line.
+__device__ __forceinline__ void sincos2(h2 th, const uint32_t *lut, h2 &sn, h2 &c) {
+  const uint32_t t = bits(th);
+  const uint32_t a0 = t & 0x7FFFu, a1 = (t >> 16) & 0x7FFFu;
+  uint32_t e0, e1;
+  if (__builtin_expect(__all(a0 <= f16tab::kLast && a1 <= f16tab::kLast), 1)) {
+    e0 = lut[a0] ^ (t & 0x8000u);          // the sign of sin(-x)
+    e1 = lut[a1] ^ ((t >> 16) & 0x8000u);
+  } else {
+    const uint64_t e = sincos2_beyond(t);
+    e0 = uint32_t(e);
+    e1 = uint32_t(e >> 32);
+  }
+  sn = of_bits(__builtin_amdgcn_perm(e1, e0, 0x05040100u));
+  c = of_bits(__builtin_amdgcn_perm(e1, e0, 0x07060302u));
+}
+
+// One explicit-Euler step of both environments, in the operation order of
+// the binary16 step (dynamics16).
+__device__ __forceinline__ S2 dynamics2(const S2 &s, h2 force, const uint32_t *lut) {
+  const h2 g = h2{half_t(9.8), half_t(9.8)}, mp = h2{half_t(0.1), half_t(0.1)};
+  const h2 l = h2{half_t(0.5), half_t(0.5)}, tau = h2{half_t(0.02), half_t(0.02)};
+  const h2 four3 = h2{half_t(4.0 / 3.0), half_t(4.0 / 3.0)};
+  const h2 pml = mp * l;
+  h2 sn, c;
+  sincos2(s.th, lut, sn, c);
+  const h2 thd2 = s.thd * s.thd;
+  const h2 c2 = c * c;
+  const h2 temp = mul_round2(force + pml * thd2 * sn, kInvTotalMass16);
+  const h2 num = g * sn - c * temp;
+  const h2 den = l * (four3 - mul_round2(mp * c2, kInvTotalMass16));
+  const h2 thacc = mul_round2(num, recip(den[0]), recip(den[1]));
+  const h2 xacc = temp - mul_round2(pml * thacc * c, kInvTotalMass16);
+  return S2{s.x + tau * s.xd, s.xd + tau * xacc, s.th + tau * s.thd, s.thd + tau * thacc};
+}
+
+__device__ __forceinline__ bool done16(half_t x, half_t th) {
+  const half_t xl = half_t(2.4), tl = half_t(kThetaLimit64);
+  return x < -xl || x > xl || th < -tl || th > tl;
+}
+
+// Start state of episode k of env into half `h` of the planes of n.
+__device__ __forceinline__ void draw_into(S2 &n, int h, U2 key, uint32_t env, uint32_t k) {
+  const State16 d = PrecF16::draw(key, env, k);
+  n.x[h] = d.x;
+  n.xd[h] = d.xd;
+  n.th[h] = d.th;
+  n.thd[h] = d.thd;
+}
+
+// The same draw out of line, for a second termination before the refill
+// (never, for episodes started from the reset distribution, which last at
+// least 8 steps): x, x_dot in the first word, theta, theta_dot in the second.
+__device__ __attribute__((noinline)) uint64_t draw_late(U2 key, uint32_t env, uint32_t k) {
+  const State16 d = PrecF16::draw(key, env, k);
+  const uint32_t w0 = uint32_t(__builtin_bit_cast(uint16_t, d.x)) |
+                      (uint32_t(__builtin_bit_cast(uint16_t, d.xd)) << 16);
+  const uint32_t w1 = uint32_t(__builtin_bit_cast(uint16_t, d.th)) |
+                      (uint32_t(__builtin_bit_cast(uint16_t, d.thd)) << 16);
+  return (static_cast<uint64_t>(w1) << 32) | w0;
+}
+
+__device__ __forceinline__ void put_late(S2 &n, int h, uint64_t w) {
+  n.x[h] = __builtin_bit_cast(half_t, uint16_t(w));
+  n.xd[h] = __builtin_bit_cast(half_t, uint16_t(w >> 16));
+  n.th[h] = __builtin_bit_cast(half_t, uint16_t(w >> 32));
+  n.thd[h] = __builtin_bit_cast(half_t, uint16_t(w >> 48));
+}
+
+// Per-half select: the planes of r where m (0xFFFF per half) is set.
+__device__ __forceinline__ h2 pick(uint32_t m, h2 r, h2 v) {
+  return of_bits((bits(r) & m) | (bits(v) & ~m));
+}
+
+template <bool kTraj>
+__global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
+  __shared__ uint32_t lut[f16tab::kEntries];
+  for (uint32_t b = threadIdx.x; b < f16tab::kEntries; b += kBlock16) lut[b] = kSinCos16.v[b];
+  __syncthreads();
+
+  const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
+  const uint32_t base = (blockIdx.x * kWaves16 + wave) * kEnvsPerWave;  // first env of the wave
+  const uint32_t i0 = base + lane, i1 = base + 64u + lane;
+  const bool v0 = i0 < p.n, v1 = i1 < p.n;
+  half_t *const px = reinterpret_cast<half_t *>(p.x);
+  half_t *const pxd = reinterpret_cast<half_t *>(p.xd);
+  half_t *const pth = reinterpret_cast<half_t *>(p.th);
+  half_t *const pthd = reinterpret_cast<half_t *>(p.thd);
+  half_t *const pobs = reinterpret_cast<half_t *>(p.obs);
+  const uint32_t e0 = p.env_base + i0, e1 = p.env_base + i1;
+  unsigned long long wave_done = 0u;
+  uint32_t returns = 0u;
+  // Waves wholly past the batch skip the loop (they still take part in the
+  // block's final reduction).
+  if (base < p.n) {
+    S2 s{h2{0, 0}, h2{0, 0}, h2{0, 0}, h2{0, 0}};
+    uint32_t k0[2] = {0u, 0u}, len0[2] = {0u, 0u};
+    if (v0) {
+      s.x[0] = px[i0]; s.xd[0] = pxd[i0]; s.th[0] = pth[i0]; s.thd[0] = pthd[i0];
+      k0[0] = p.ep_index[i0];
+      len0[0] = p.ep_len[i0];
+    }
+    if (v1) {
+      s.x[1] = px[i1]; s.xd[1] = pxd[i1]; s.th[1] = pth[i1]; s.thd[1] = pthd[i1];
+      k0[1] = p.ep_index[i1];
+      len0[1] = p.ep_len[i1];
+    }
+    uint32_t k[2] = {k0[0], k0[1]}, len[2] = {len0[0], len0[1]};
+    // next start states, drawn ahead of time; have[h]: drawn for half h
+    S2 nxt;
+    draw_into(nxt, 0, p.krst, e0, k[0] + 1u);
+    draw_into(nxt, 1, p.krst, e1, k[1] + 1u);
+    bool have0 = true, have1 = true;
+    // random actions: the wave's two 64-environment blocks; every 64 steps
+    // lane L computes both blocks' words of step tb + L
+    const uint32_t g0 = uint32_t(__builtin_amdgcn_readfirstlane(int(e0))) >> 6;
+    U2 b0{0u, 0u}, b1{0u, 0u};
+    uint32_t tb = 0u;
+    auto step = [&](uint32_t j) {
+      const uint32_t t = p.t0 + j;
+      if (j == 0u || (t & 63u) == 0u) {
+        tb = t & ~63u;
+        b0 = threefry2x32(p.kact.a, p.kact.b, g0, tb + lane);
+        b1 = threefry2x32(p.kact.a, p.kact.b, g0 + 1u, tb + lane);
+      }
+      const int src = int(t - tb);
+      const unsigned long long w0 =
+          (static_cast<unsigned long long>(uint32_t(__builtin_amdgcn_readlane(int(b0.b), src)))
+           << 32) | uint32_t(__builtin_amdgcn_readlane(int(b0.a), src));
+      const unsigned long long w1 =
+          (static_cast<unsigned long long>(uint32_t(__builtin_amdgcn_readlane(int(b1.b), src)))
+           << 32) | uint32_t(__builtin_amdgcn_readlane(int(b1.a), src));
+      const bool a0 = __builtin_amdgcn_inverse_ballot_w64(w0);
+      const bool a1 = __builtin_amdgcn_inverse_ballot_w64(w1);
+      const h2 force = h2{a0 ? half_t(10.0) : half_t(-10.0), a1 ? half_t(10.0) : half_t(-10.0)};
+      S2 o = dynamics2(s, force, lut);
+      const bool d0 = v0 && done16(o.x[0], o.th[0]);
+      const bool d1 = v1 && done16(o.x[1], o.th[1]);
+      k[0] += d0 ? 1u : 0u;
+      k[1] += d1 ? 1u : 0u;
+      len[0] = d0 ? 0u : len[0] + 1u;
+      len[1] = d1 ? 0u : len[1] + 1u;
+      // a second termination before the refill draws its start state now
+      if (d0 && !have0) put_late(nxt, 0, draw_late(p.krst, e0, k[0]));
+      if (d1 && !have1) put_late(nxt, 1, draw_late(p.krst, e1, k[1]));
+      const uint32_t m = (d0 ? 0x0000FFFFu : 0u) | (d1 ? 0xFFFF0000u : 0u);
+      o.x = pick(m, nxt.x, o.x);
+      o.xd = pick(m, nxt.xd, o.xd);
+      o.th = pick(m, nxt.th, o.th);
+      o.thd = pick(m, nxt.thd, o.thd);
+      have0 = have0 && !d0;
+      have1 = have1 && !d1;
+      s = o;
+      if (kTraj) {
+        const size_t plane = size_t(j) * p.n;
+        if (p.obs) {
+          half_t *const ob = pobs + 4u * plane;
+          if (v0) {
+            ob[i0] = s.x[0]; ob[p.n + i0] = s.xd[0];
+            ob[2u * size_t(p.n) + i0] = s.th[0]; ob[3u * size_t(p.n) + i0] = s.thd[0];
+          }
+          if (v1) {
+            ob[i1] = s.x[1]; ob[p.n + i1] = s.xd[1];
+            ob[2u * size_t(p.n) + i1] = s.th[1]; ob[3u * size_t(p.n) + i1] = s.thd[1];
+          }
+        }
+        if (p.reward) {
+          if (v0) p.reward[plane + i0] = 1.0f;
+          if (v1) p.reward[plane + i1] = 1.0f;
+        }
+        if (p.done) {
+          if (v0) p.done[plane + i0] = uint8_t(d0);
+          if (v1) p.done[plane + i1] = uint8_t(d1);
+        }
+      }
+      wave_done += __popcll(__ballot(d0)) + __popcll(__ballot(d1));
+    };
+    uint32_t j = 0;
+    for (; j + kRefill <= p.T; j += kRefill) {
+#pragma unroll
+      for (uint32_t r = 0; r < kRefill; ++r) step(j + r);
+      if (!have0) {
+        draw_into(nxt, 0, p.krst, e0, k[0] + 1u);
+        have0 = true;
+      }
+      if (!have1) {
+        draw_into(nxt, 1, p.krst, e1, k[1] + 1u);
+        have1 = true;
+      }
+    }
+    for (; j < p.T; ++j) step(j);
+    // as the one-per-lane kernel: terminations are the growth of the episode
+    // index, finished returns T + len(start) - len(end)
+    const bool v[2] = {v0, v1};
+    const uint32_t ii[2] = {i0, i1};
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      if (!v[h]) continue;
+      const uint32_t i = ii[h];
+      const uint32_t n_done = k[h] - k0[h], ret = p.T + len0[h] - len[h];
+      returns += ret;
+      px[i] = s.x[h];
+      pxd[i] = s.xd[h];
+      pth[i] = s.th[h];
+      pthd[i] = s.thd[h];
+      p.ep_index[i] = k[h];
+      p.ep_len[i] = len[h];
+      if (p.done_count) p.done_count[i] = (p.first ? 0u : p.done_count[i]) + n_done;
+      if (p.total_reward) {
+        const float prev = p.first ? 0.0f : p.total_reward[i];
+        const float cap = float(1u << 24);
+        p.total_reward[i] = prev >= cap ? prev : __builtin_fminf(prev + float(p.T), cap);
+      }
+      if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
+    }
+  }
+  if (p.global) block_publish<kBlock16>(p.global, wave_done, returns, true);
+}
+
+}  // namespace
+
+bool resident_f16x2_applies(const RolloutParams &p) { return p.env_base % 64u == 0u; }
+
+hipError_t launch_resident_f16x2(const RolloutParams &p, hipStream_t stream) {
+  const uint32_t per_block = kBlock16 * 2u;
+  const dim3 grid((p.n + per_block - 1u) / per_block);
+  const bool traj = p.obs || p.reward || p.done;
+  if (traj)
+    hipLaunchKernelGGL(k_resident_f16x2<true>, grid, dim3(kBlock16), 0, stream, p);
+  else
+    hipLaunchKernelGGL(k_resident_f16x2<false>, grid, dim3(kBlock16), 0, stream, p);
+  return hipGetLastError();
+}
+
+}  // namespace cp

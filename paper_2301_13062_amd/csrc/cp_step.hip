@@ -54,19 +54,16 @@ __global__ __launch_bounds__(kBlock) void k_init(typename P::T *__restrict__ x,
   ep_len[i] = 0u;
 }
 
-// Stores of one environment's step: the state (unless the trajectory's obs
-// plane holds it), the running episode length, the step outputs and the
-// rollout accumulators.  kOff32: as for elem(), for every array written
-// (each obs plane addressed from its own base).
+// Stores of one environment's step: the state, the running episode length,
+// the step outputs and the rollout accumulators.  kOff32: as for elem(), for
+// every array written (each obs plane addressed from its own base).
 template <bool kOff32 = false>
 __device__ __forceinline__ void store_step(const StepParams &p, uint32_t i, const State &o,
                                            uint32_t len, uint32_t d, uint32_t ret) {
-  if (p.x) {
-    *elem<kOff32>(p.x, i) = o.x;
-    *elem<kOff32>(p.xd, i) = o.xd;
-    *elem<kOff32>(p.th, i) = o.th;
-    *elem<kOff32>(p.thd, i) = o.thd;
-  }
+  *elem<kOff32>(p.x, i) = o.x;
+  *elem<kOff32>(p.xd, i) = o.xd;
+  *elem<kOff32>(p.th, i) = o.th;
+  *elem<kOff32>(p.thd, i) = o.thd;
   *elem<kOff32>(p.ep_len, i) = len;
   if (p.obs) {
     __builtin_nontemporal_store(o.x, elem<kOff32>(p.obs, i));
@@ -137,25 +134,104 @@ __device__ __forceinline__ void fused_rest(const StepParams &p, uint32_t i, uint
   store_step<kOff32>(p, i, o, len, d, ret);
 }
 
-// kStream: the step reads its state from other arrays than it writes (the
-// previous obs plane of a trajectory rollout), which nothing reads again;
-// non-temporal loads keep those lines out of the caches (measured: 135 ->
-// 129 us per launch at 16,777,216 environments, while for a step that
-// rewrites the arrays it reads they cost 15%).
-template <bool kExplicit, bool kEager, bool kStream = false, bool kOff32 = false>
+template <bool kExplicit, bool kEager, bool kOff32 = false>
 __device__ __forceinline__ void fused_one(const StepParams &p, uint32_t i, uint32_t a) {
-  State s;
-  if (kStream)
-    s = State{__builtin_nontemporal_load(elem<kOff32>(p.xi, i)),
-              __builtin_nontemporal_load(elem<kOff32>(p.xdi, i)),
-              __builtin_nontemporal_load(elem<kOff32>(p.thi, i)),
-              __builtin_nontemporal_load(elem<kOff32>(p.thdi, i))};
-  else
-    s = State{*elem<kOff32>(p.xi, i), *elem<kOff32>(p.xdi, i), *elem<kOff32>(p.thi, i),
-              *elem<kOff32>(p.thdi, i)};
+  const State s{*elem<kOff32>(p.xi, i), *elem<kOff32>(p.xdi, i), *elem<kOff32>(p.thi, i),
+                *elem<kOff32>(p.thdi, i)};
   if (kExplicit) a = uint32_t(*elem<kOff32>(p.actions, i) != 0);
   fused_rest<kEager, kOff32>(p, i, a, s, *elem<kOff32>(p.ep_len, i),
                              kEager ? *elem<kOff32>(p.ep_index, i) : 0u);
+}
+
+// Streaming rollout (bandwidth-bound batches writing the obs trajectory,
+// random actions): step j reads its state from the previous step's obs plane
+// (the state arrays at j = 0) with non-temporal loads -- nothing reads those
+// lines again (measured: 135 -> 129 us per launch at 16,777,216
+// environments, while for a step that rewrites the arrays it reads they cost
+// 15%).  The episode counters are not carried through every step: a step
+// touches them only where an environment terminates -- the episode index
+// read, incremented and written back, the episode length overwritten with
+// the step's index j -- and the last step rebuilds them.  Between the first
+// and the last step the state arrays hold no state (the trajectory does),
+// so the first step parks each environment's starting episode index and
+// length in x and x_dot; the last step reads them back, and from them and
+// the counters derives the final episode length (0 if it terminated at the
+// last step, j - (step of its last termination) if it terminated earlier
+// in the rollout, start length + T otherwise), the per-environment
+// statistics (terminations: index growth; finished returns: T + start
+// length - final length) and writes the final state.  Per intermediate step
+// that is 16 B read and 21 B written per environment plus 8 B read and
+// written at terminations only, against 8 B read and written every step for
+// a carried length (measured 123.4 -> 113.0 us per launch).
+enum class Phase { kFirst, kMid, kLast };
+
+template <Phase kPhase, bool kOff32>
+__global__ __launch_bounds__(kBlock) void k_stream_step(StepParams p, uint32_t j, uint32_t T,
+                                                        unsigned long long *global) {
+  const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+  const uint32_t a = action_bit_wave(p.kact, p.env_base + i, p.t);
+  uint32_t n_done = 0u, ret = 0u;  // the last step's per-environment totals
+  if (i < p.n) {
+    const State s{__builtin_nontemporal_load(elem<kOff32>(p.xi, i)),
+                  __builtin_nontemporal_load(elem<kOff32>(p.xdi, i)),
+                  __builtin_nontemporal_load(elem<kOff32>(p.thi, i)),
+                  __builtin_nontemporal_load(elem<kOff32>(p.thdi, i))};
+    // The starting counters are parked in x and x_dot as binary32 bit
+    // patterns (stores and loads move the bits unchanged), through the
+    // arrays' own type so that they stay ordered after this lane's loads of
+    // x[i] and x_dot[i] and before its final stores.
+    uint32_t k0 = 0u, len0 = 0u, kprev = 0u;
+    if (kPhase == Phase::kFirst) {
+      k0 = *elem<kOff32>(p.ep_index, i);
+      len0 = *elem<kOff32>(p.ep_len, i);
+      *elem<kOff32>(p.x, i) = __builtin_bit_cast(float, k0);
+      *elem<kOff32>(p.xd, i) = __builtin_bit_cast(float, len0);
+    }
+    if (kPhase == Phase::kLast) kprev = *elem<kOff32>(p.ep_index, i);
+    State o = dynamics(s, force_of(a));
+    const uint32_t d = terminated(o) ? 1u : 0u;
+    if (d) {
+      uint32_t k;
+      if (kPhase == Phase::kFirst) k = k0 + 1u;
+      else if (kPhase == Phase::kLast) k = kprev + 1u;
+      else k = *elem<kOff32>(p.ep_index, i) + 1u;
+      if (kPhase != Phase::kLast) {
+        *elem<kOff32>(p.ep_index, i) = k;
+        *elem<kOff32>(p.ep_len, i) = j;  // step of the latest termination
+      }
+      o = reset_draw(p.krst, p.env_base + i, k);
+    }
+    __builtin_nontemporal_store(o.x, elem<kOff32>(p.obs, i));
+    __builtin_nontemporal_store(o.xd, elem<kOff32>(p.obs + size_t(p.n), i));
+    __builtin_nontemporal_store(o.th, elem<kOff32>(p.obs + 2u * size_t(p.n), i));
+    __builtin_nontemporal_store(o.thd, elem<kOff32>(p.obs + 3u * size_t(p.n), i));
+    if (p.reward) __builtin_nontemporal_store(1.0f, elem<kOff32>(p.reward, i));
+    if (p.done) __builtin_nontemporal_store(uint8_t(d), elem<kOff32>(p.done, i));
+    if (kPhase == Phase::kLast) {
+      k0 = __builtin_bit_cast(uint32_t, float(*elem<kOff32>(p.x, i)));
+      len0 = __builtin_bit_cast(uint32_t, float(*elem<kOff32>(p.xd, i)));
+      const uint32_t k_end = kprev + d;
+      uint32_t len_end;
+      if (d) len_end = 0u;
+      else if (kprev != k0) len_end = j - *elem<kOff32>(p.ep_len, i);
+      else len_end = len0 + T;
+      *elem<kOff32>(p.x, i) = o.x;  // the final state replaces the slots
+      *elem<kOff32>(p.xd, i) = o.xd;
+      *elem<kOff32>(p.th, i) = o.th;
+      *elem<kOff32>(p.thd, i) = o.thd;
+      *elem<kOff32>(p.ep_index, i) = k_end;
+      *elem<kOff32>(p.ep_len, i) = len_end;
+      // this rollout's terminations and finished returns, modulo 2^32 like
+      // the counters themselves
+      n_done = k_end - k0;
+      ret = T + len0 - len_end;
+      if (p.done_count) *elem<kOff32>(p.done_count, i) = n_done;
+      if (p.total_reward)
+        *elem<kOff32>(p.total_reward, i) = T >= (1u << 24) ? float(1u << 24) : float(T);
+      if (p.ret_sum) *elem<kOff32>(p.ret_sum, i) = ret;
+    }
+  }
+  if (kPhase == Phase::kLast && global) block_publish<kBlock>(global, n_done, ret, false);
 }
 
 // Concatenated-state level (the paper's baseline before its "no concat"
@@ -195,12 +271,12 @@ __global__ __launch_bounds__(kBlock) void k_concat_finish(StepParams p, const f3
 
 // kOff32 is launched only below kOff32MaxEnvs environments (kEager, below
 // kEagerMaxEnvs, always is).
-template <bool kExplicit, bool kEager, bool kStream, bool kOff32>
+template <bool kExplicit, bool kEager, bool kOff32>
 __global__ __launch_bounds__(kBlock) void k_fused_step(StepParams p) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
   // random actions: one block per wave, before any lane leaves
   const uint32_t a = kExplicit ? 0u : action_bit_wave(p.kact, p.env_base + i, p.t);
-  if (i < p.n) fused_one<kExplicit, kEager, kStream, kOff32>(p, i, a);
+  if (i < p.n) fused_one<kExplicit, kEager, kOff32>(p, i, a);
 }
 
 // Horizontal fusion (the paper's horizontal fusion pass, Sec. "Fusion
@@ -217,11 +293,11 @@ __global__ __launch_bounds__(kBlock) void k_group_step(GroupParams g) {
   const StepParams &p = g.p[m];
   const uint32_t i = (blockIdx.x - g.first_block[m]) * kBlock + threadIdx.x;
   if (p.actions) {
-    if (i < p.n) fused_one<true, true, false, false>(p, i, 0u);
+    if (i < p.n) fused_one<true, true, false>(p, i, 0u);
   } else {
     // random actions: one block per wave, before any lane leaves
     const uint32_t a = action_bit_wave(p.kact, p.env_base + i, p.t);
-    if (i < p.n) fused_one<false, true, false, false>(p, i, a);
+    if (i < p.n) fused_one<false, true, false>(p, i, a);
   }
 }
 
@@ -475,20 +551,34 @@ hipError_t launch_fused_step(const StepParams &p, hipStream_t stream) {
   const dim3 g = grid_for(p.n), b(kBlock);
   const bool eager = p.n < kEagerMaxEnvs, off32 = p.n < kOff32MaxEnvs;
   if (p.actions) {
-    if (eager) hipLaunchKernelGGL((k_fused_step<true, true, false, true>), g, b, 0, stream, p);
-    else if (off32)
-      hipLaunchKernelGGL((k_fused_step<true, false, false, true>), g, b, 0, stream, p);
-    else hipLaunchKernelGGL((k_fused_step<true, false, false, false>), g, b, 0, stream, p);
+    if (eager) hipLaunchKernelGGL((k_fused_step<true, true, true>), g, b, 0, stream, p);
+    else if (off32) hipLaunchKernelGGL((k_fused_step<true, false, true>), g, b, 0, stream, p);
+    else hipLaunchKernelGGL((k_fused_step<true, false, false>), g, b, 0, stream, p);
   } else if (eager) {
-    hipLaunchKernelGGL((k_fused_step<false, true, false, true>), g, b, 0, stream, p);
-  } else if (p.xi != p.x) {  // state read from elsewhere than it is written
-    if (off32) hipLaunchKernelGGL((k_fused_step<false, false, true, true>), g, b, 0, stream, p);
-    else hipLaunchKernelGGL((k_fused_step<false, false, true, false>), g, b, 0, stream, p);
+    hipLaunchKernelGGL((k_fused_step<false, true, true>), g, b, 0, stream, p);
   } else if (off32) {
-    hipLaunchKernelGGL((k_fused_step<false, false, false, true>), g, b, 0, stream, p);
+    hipLaunchKernelGGL((k_fused_step<false, false, true>), g, b, 0, stream, p);
   } else {
-    hipLaunchKernelGGL((k_fused_step<false, false, false, false>), g, b, 0, stream, p);
+    hipLaunchKernelGGL((k_fused_step<false, false, false>), g, b, 0, stream, p);
   }
+  return hipGetLastError();
+}
+
+template <Phase kPhase>
+static void stream_as(const StepParams &p, uint32_t j, uint32_t T,
+                      unsigned long long *global, hipStream_t stream) {
+  const dim3 g = grid_for(p.n), b(kBlock);
+  if (p.n < kOff32MaxEnvs)
+    hipLaunchKernelGGL((k_stream_step<kPhase, true>), g, b, 0, stream, p, j, T, global);
+  else
+    hipLaunchKernelGGL((k_stream_step<kPhase, false>), g, b, 0, stream, p, j, T, global);
+}
+
+hipError_t launch_stream_step(const StepParams &p, uint32_t j, uint32_t T,
+                              unsigned long long *global, hipStream_t stream) {
+  if (j == 0u) stream_as<Phase::kFirst>(p, j, T, nullptr, stream);
+  else if (j + 1u == T) stream_as<Phase::kLast>(p, j, T, global, stream);
+  else stream_as<Phase::kMid>(p, j, T, nullptr, stream);
   return hipGetLastError();
 }
 
@@ -573,6 +663,8 @@ hipError_t launch_resident(const RolloutParams &p, hipStream_t stream) {
   if (p.policy_w) return launch_resident_policy(p, stream);
   if (p.precision == 1)
     resident_as<PrecF64>(p, stream);
+  else if (p.precision == 2 && resident_f16x2_applies(p))
+    return launch_resident_f16x2(p, stream);
   else if (p.precision == 2)
     resident_as<PrecF16>(p, stream);
   else

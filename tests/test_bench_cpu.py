@@ -51,7 +51,8 @@ def test_peaks_and_algorithmic_figures():
     assert bench.HBM_PEAK_GBS == 8000.0
     assert bench.VALU_PEAK_TOPS == pytest.approx(78.6432)
     assert bench.STEP_BYTES_WITH_OUTPUTS == 20 + 20 + 16 + 4 + 1
-    assert bench.STEP_BYTES_TRAJ_LARGE == 20 + 25
+    assert bench.STEP_BYTES_STREAM == 16 + 16 + 4 + 1
+    assert bench.stream_bytes_per_env_step(0.045, 100) == pytest.approx(37 + 12 * 0.045 + 0.56)
     assert bench.STEP_BYTES_TRAJ_RESIDENT == 16 + 4 + 1
     assert bench.POLICY_FLOPS == 2 * (4 * 64 + 64 * 64 + 64 * 2)
     json.dumps(bench.COUNTERS)  # plain data
@@ -64,7 +65,7 @@ def test_headline_line_shape():
     # the streaming workload in config, the roofline of the streaming kernel
     head = {"envs": 1 << 24, "steps_per_rollout": 100, "rollouts": 20, "wall_ms": 260.0,
             "event_ms": 255.0, "env_steps_per_s": (1 << 24) * 100 * 20 / 0.26,
-            "ms_per_rollout": 13.0, "kernel_mean_us": 127.5}
+            "ms_per_rollout": 13.0, "kernel_mean_us": 127.5, "termination_rate": 0.045}
     line = bench.headline_line(head, 20, 5)
     assert line["value"] == head["env_steps_per_s"] and line["unit"] == "env-steps/s"
     assert line["steps"] == 20 and line["warmup"] == 5 and line["n_gpus"] == 1
@@ -72,7 +73,9 @@ def test_headline_line_shape():
     assert "16,777,216 envs x 100 steps" in line["config"]["workload"]
     r = line["roofline"]
     assert r["bound"] == "hbm" and r["unit"] == "GB/s" and r["peak"] == 8000.0
-    assert r["achieved"] == pytest.approx(45 * (1 << 24) / 127.5e-6 / 1e9)
+    bpe = 37 + 12 * 0.045 + 56 / 100
+    assert r["bytes_per_env_step"] == pytest.approx(bpe)
+    assert r["achieved"] == pytest.approx(bpe * (1 << 24) / 127.5e-6 / 1e9)
     assert r["frac"] == pytest.approx(r["achieved"] / 8000.0)
     assert r["launches_timed"] == 2000
     json.dumps(line)

@@ -328,17 +328,21 @@ def test_large_batch_fused_trajectory_equals_resident(gpu):
     assert torch.equal(ft.obs[-1], fs.state())
 
 
-@pytest.mark.parametrize("case", ["done_planes", "with_stats", "no_done", "one_step", "long_episodes"])
+@pytest.mark.parametrize("case", ["done_planes", "with_stats", "no_done", "one_step", "two_steps",
+                                  "long_episodes", "high_episode_index"])
 def test_large_batch_episode_lengths_equal_resident(gpu, case):
-    # From 2^21 environments the fused rollout reads each step's state from
-    # the previous obs plane; with or without done flags and per-environment
-    # statistics, the episode counters, the totals and the trajectory equal
-    # the resident kernel's bit for bit -- also for one step, and for
+    # From 2^21 environments the fused rollout streams: each step reads its
+    # state from the previous obs plane and touches the episode counters only
+    # at terminations, the last step rebuilding them.  With or without done
+    # flags and per-environment statistics, the episode counters, the totals
+    # and the trajectory equal the resident kernel's bit for bit -- also for
+    # one step (no streaming) and two (first and last step only), for
     # caller-loaded lengths near the top of the u32 range (some of which
-    # wrap).
+    # wrap) and for episode indices that wrap past 2^32 - 1.
     n = (1 << 21) + 37
-    T = 1 if case == "one_step" else 20
-    kw = dict(stats=case == "with_stats", done=case != "no_done")
+    T = {"one_step": 1, "two_steps": 2}.get(case, 20)
+    kw = dict(stats=case in ("with_stats", "two_steps", "high_episode_index"),
+              done=case != "no_done")
 
     def go(variant):
         s = cp.CartPoleStates(n, variant=variant)
@@ -347,6 +351,10 @@ def test_large_batch_episode_lengths_equal_resident(gpu, case):
             g = torch.Generator(device="cuda").manual_seed(1)
             s.ep_len.copy_(torch.randint(-(1 << 31), 1 << 31, (n,), dtype=torch.int32,
                                          device="cuda", generator=g))
+        if case == "high_episode_index":
+            g = torch.Generator(device="cuda").manual_seed(2)
+            s.ep_index.copy_(torch.randint(-3, 0, (n,), dtype=torch.int32, device="cuda",
+                                           generator=g))
         tr = cp.Trajectory(n, T, **kw)
         cp.cp_rollout(s, T, 9, tr)
         torch.cuda.synchronize()

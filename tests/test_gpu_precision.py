@@ -208,3 +208,54 @@ def test_rollout_1m_x_1000_sampled(gpu, prec):
     else:
         assert same.mean() >= ROLL_MATCH
         assert np.abs(g[:, ids][:, same] - o.state()[:, same]).max() <= ROLL64_ABS
+
+
+def _f16_equal(g, o):
+    """binary16 arrays equal bit for bit, any NaN matching any NaN."""
+    g, o = np.asarray(g, np.float16), np.asarray(o, np.float16)
+    gn, on = np.isnan(g), np.isnan(o)
+    return np.array_equal(gn, on) and np.array_equal(g.view(np.uint16)[~gn], o.view(np.uint16)[~on])
+
+
+@pytest.mark.parametrize("env_base", [0, 64, 5])
+def test_f16_wide_states_both_kernel_forms(gpu, env_base):
+    # binary16 with the launch's first environment a multiple of 64 (two
+    # environments per lane: table sin/cos, one-rounding divisions) and not
+    # (one per lane), from states the library never produces -- angles up to
+    # 1.5 rad (beyond the table), NaN and infinite values, subnormals, zeros
+    # of both signs -- then 30 steps on from them: bit for bit as the oracle.
+    n, T = 3000 + 77, 30
+    rng = np.random.default_rng(17 + env_base)
+    st4 = synth.states(n, seed=23, kind="adversarial").astype(np.float16)
+    pick = rng.random(n)
+    st4[2, pick < 0.3] = rng.uniform(-1.5, 1.5, int((pick < 0.3).sum())).astype(np.float16)
+    st4[2, (pick >= 0.3) & (pick < 0.32)] = np.nan
+    st4[0, (pick >= 0.32) & (pick < 0.34)] = np.inf
+    st4[3, (pick >= 0.34) & (pick < 0.36)] = np.float16(2.0 ** -20)
+    st4[2, (pick >= 0.36) & (pick < 0.38)] = np.float16(-0.0)
+    st4[2, (pick >= 0.38) & (pick < 0.40)] = np.float16(-(2.0 ** -24))
+    ep_index = rng.integers(0, 1000, n).astype(np.uint32)
+    ep_len = rng.integers(0, 300, n).astype(np.uint32)
+    for steps in (1, T):
+        s = handle(n, "f16", env_base)
+        for dst, src in zip((s.x, s.x_dot, s.theta, s.theta_dot), st4):
+            dst.copy_(torch.from_numpy(np.ascontiguousarray(src)))
+        s.ep_index.copy_(torch.from_numpy(ep_index.view(np.int32)))
+        s.ep_len.copy_(torch.from_numpy(ep_len.view(np.int32)))
+        s.seed, s.t = 12, 345
+        tr = traj(n, steps, "f16")
+        cp.cp_rollout(s, steps, 99, tr)
+        torch.cuda.synchronize()
+        o = oracle_state(n, "f16", np.arange(env_base, env_base + n))
+        o.x, o.x_dot, o.theta, o.theta_dot = (np.ascontiguousarray(v) for v in st4)
+        o.ep_index, o.ep_len = ep_index.copy(), ep_len.copy()
+        o.seed, o.t = 12, 345
+        out = O.rollout_prec(o, steps, act_seed=99, traj=True)
+        g, gk, gl = gpu_state(s)
+        assert np.array_equal(tr.done.cpu().numpy(), out["done"]), steps
+        assert _f16_equal(tr.obs.cpu().numpy(), out["obs"]), steps
+        assert _f16_equal(g, o.state()), steps
+        assert np.array_equal(gk, o.ep_index) and np.array_equal(gl, o.ep_len)
+        for f in ("done_count", "ret_sum"):
+            assert np.array_equal(getattr(tr, f).cpu().numpy().view(np.uint32), out[f]), f
+        assert int(tr.totals[0]) == int(out["done_count"].sum())
