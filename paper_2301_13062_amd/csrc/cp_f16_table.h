@@ -99,5 +99,26 @@ constexpr Table make_table() {
   return t;
 }
 
+// The binary32 reciprocals RN32(1/d) of the divisors d of the binary16
+// step's angular acceleration, d = l (4/3 - mp c^2 / M) rounded as the step
+// rounds it: for every cosine c in [-1, 1] these are the 94 binary16 values
+// with bit patterns 0x38F8 .. 0x3955 (0.62109375 .. 0.66650390625).  The
+// binary64 quotient is within 2^-53 of 1/d, and 1/d of an 11-bit d is never
+// that close to a binary32 rounding boundary, so converting it rounds 1/d
+// correctly.
+constexpr uint32_t kDenFirst = 0x38F8u, kDenLast = 0x3955u;
+constexpr uint32_t kDenEntries = kDenLast - kDenFirst + 1u;
+
+struct RecipTable {
+  float v[kDenEntries];
+};
+
+constexpr RecipTable make_recip_table() {
+  RecipTable t{};
+  for (uint32_t b = kDenFirst; b <= kDenLast; ++b)
+    t.v[b - kDenFirst] = static_cast<float>(1.0 / value_of(b));
+  return t;
+}
+
 }  // namespace f16tab
 }  // namespace cp

@@ -17,13 +17,20 @@
 //    correctly rounded quotient for every binary16 a, the exact quotients
 //    lying at least 2^-21 (relative) from a binary16 rounding boundary while
 //    RN32(1/m) is within 2^-24 of 1/m;
-//  * the angular acceleration num / den is num times the binary32
-//    reciprocal of den (refined by one Newton step: within 2^-24 (1 + 2^-22)
-//    relative), rounded once the same way: every divisor the step can form
-//    lies in [0.621, 0.667] (94 binary16 values), and for each of them every
-//    binary16 quotient lies at least 2^-22.4 from a rounding boundary.
+//  * the angular acceleration num / den is num times RN32(1/den), rounded
+//    once the same way: every divisor the step can form is one of 94
+//    binary16 values (0.621 .. 0.667), whose reciprocals sit in a second LDS
+//    table, and for each of them every binary16 quotient lies at least
+//    2^-22.4 (relative) from a rounding boundary, farther than RN32(1/den)
+//    is from 1/den (2^-24).
+// States a step produces hold angles within the 12-degree limit or NaN, so
+// only a launch's first step can meet an angle beyond the table: it is
+// peeled off the loop, and the loop's steps read the table alone (NaN
+// angles reading an entry of NaNs).
 // The actions of a wave's 128 environments are two 64-environment blocks of
 // the random stream, each a lane mask (one select per environment).
+#include <type_traits>
+
 #include "cp_f16_table.h"
 #include "cp_launch.h"
 #include "cp_resident.h"
@@ -38,8 +45,13 @@ constexpr int kBlock16 = 1024;  // 16 waves share one LDS copy of the table
 constexpr int kWaves16 = kBlock16 / 64;
 constexpr uint32_t kEnvsPerWave = 128u;
 
-// The table, evaluated at compile time.
+// The tables, evaluated at compile time.
 __device__ const f16tab::Table kSinCos16 = f16tab::make_table();
+__device__ const f16tab::RecipTable kRecipDen16 = f16tab::make_recip_table();
+// LDS layout: the sin/cos entries, then one entry of two NaNs (for NaN
+// angles), then the divisor reciprocals.
+constexpr uint32_t kNanEntry = f16tab::kEntries;
+constexpr uint32_t kLutWords = f16tab::kEntries + 1u + f16tab::kDenEntries;
 
 __device__ __forceinline__ uint32_t bits(h2 v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ h2 of_bits(uint32_t u) { return __builtin_bit_cast(h2, u); }
@@ -65,13 +77,13 @@ __device__ __forceinline__ h2 mul_round2(h2 a, float c0, float c1) {
   return of_bits(r);
 }
 
-// The binary32 reciprocal of a binary16 divisor, one Newton step after the
-// hardware estimate.
-__device__ __forceinline__ float recip(_Float16 d) {
-  const float b = float(d);
-  const float y0 = __builtin_amdgcn_rcpf(b);
-  const float e = __builtin_fmaf(-b, y0, 1.0f);
-  return __builtin_fmaf(e, y0, y0);
+// RN32(1/d) for a divisor of the angular acceleration (bits b of one
+// binary16 d), from the LDS table; a NaN divisor (only with a NaN angle,
+// whose numerator is NaN too) reads the last entry.
+__device__ __forceinline__ float recip(uint32_t b, const uint32_t *lut) {
+  const uint32_t k = b - f16tab::kDenFirst;  // wraps to large for b < kDenFirst
+  const uint32_t idx = k < f16tab::kDenEntries - 1u ? k : f16tab::kDenEntries - 1u;
+  return __builtin_bit_cast(float, lut[kNanEntry + 1u + idx]);
 }
 
 struct S2 {
@@ -93,14 +105,20 @@ __device__ __attribute__((noinline)) uint64_t sincos2_beyond(uint32_t t) {
   return (static_cast<uint64_t>(e1) << 32) | e0;
 }
 
-// sin and cos of both angles of th: from the table when every lane's angles
-// are at most 1/4 in magnitude, else for the whole wave out of line.
+// sin and cos of both angles of th.  kAny: any angle (a launch's first
+// step): from the table when every lane's angles are at most 1/4 in
+// magnitude, else for the whole wave out of line.  Otherwise the angle is
+// within the limit or NaN: the table alone, NaN reading the entry of NaNs.
+template <bool kAny>
 __device__ __forceinline__ void sincos2(h2 th, const uint32_t *lut, h2 &sn, h2 &c) {
   const uint32_t t = bits(th);
   const uint32_t a0 = t & 0x7FFFu, a1 = (t >> 16) & 0x7FFFu;
   uint32_t e0, e1;
-  if (__builtin_expect(__all(a0 <= f16tab::kLast && a1 <= f16tab::kLast), 1)) {
-    e0 = lut[a0] ^ (t & 0x8000u);          // the sign of sin(-x)
+  if (!kAny) {
+    e0 = lut[a0 <= f16tab::kLast ? a0 : kNanEntry] ^ (t & 0x8000u);  // the sign of sin(-x)
+    e1 = lut[a1 <= f16tab::kLast ? a1 : kNanEntry] ^ ((t >> 16) & 0x8000u);
+  } else if (__all(a0 <= f16tab::kLast && a1 <= f16tab::kLast)) {
+    e0 = lut[a0] ^ (t & 0x8000u);
     e1 = lut[a1] ^ ((t >> 16) & 0x8000u);
   } else {
     const uint64_t e = sincos2_beyond(t);
@@ -113,19 +131,21 @@ __device__ __forceinline__ void sincos2(h2 th, const uint32_t *lut, h2 &sn, h2 &
 
 // One explicit-Euler step of both environments, in the operation order of
 // the binary16 step (dynamics16).
+template <bool kAny>
 __device__ __forceinline__ S2 dynamics2(const S2 &s, h2 force, const uint32_t *lut) {
   const h2 g = h2{half_t(9.8), half_t(9.8)}, mp = h2{half_t(0.1), half_t(0.1)};
   const h2 l = h2{half_t(0.5), half_t(0.5)}, tau = h2{half_t(0.02), half_t(0.02)};
   const h2 four3 = h2{half_t(4.0 / 3.0), half_t(4.0 / 3.0)};
   const h2 pml = mp * l;
   h2 sn, c;
-  sincos2(s.th, lut, sn, c);
+  sincos2<kAny>(s.th, lut, sn, c);
   const h2 thd2 = s.thd * s.thd;
   const h2 c2 = c * c;
   const h2 temp = mul_round2(force + pml * thd2 * sn, kInvTotalMass16);
   const h2 num = g * sn - c * temp;
   const h2 den = l * (four3 - mul_round2(mp * c2, kInvTotalMass16));
-  const h2 thacc = mul_round2(num, recip(den[0]), recip(den[1]));
+  const uint32_t db = bits(den);
+  const h2 thacc = mul_round2(num, recip(db & 0xFFFFu, lut), recip(db >> 16, lut));
   const h2 xacc = temp - mul_round2(pml * thacc * c, kInvTotalMass16);
   return S2{s.x + tau * s.xd, s.xd + tau * xacc, s.th + tau * s.thd, s.thd + tau * thacc};
 }
@@ -170,8 +190,11 @@ __device__ __forceinline__ h2 pick(uint32_t m, h2 r, h2 v) {
 
 template <bool kTraj>
 __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
-  __shared__ uint32_t lut[f16tab::kEntries];
-  for (uint32_t b = threadIdx.x; b < f16tab::kEntries; b += kBlock16) lut[b] = kSinCos16.v[b];
+  __shared__ uint32_t lut[kLutWords];
+  for (uint32_t b = threadIdx.x; b < kLutWords; b += kBlock16)
+    lut[b] = b < f16tab::kEntries ? kSinCos16.v[b]
+             : b == kNanEntry     ? 0x7E007E00u
+                                  : __builtin_bit_cast(uint32_t, kRecipDen16.v[b - kNanEntry - 1u]);
   __syncthreads();
 
   const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
@@ -212,7 +235,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
     const uint32_t g0 = uint32_t(__builtin_amdgcn_readfirstlane(int(e0))) >> 6;
     U2 b0{0u, 0u}, b1{0u, 0u};
     uint32_t tb = 0u;
-    auto step = [&](uint32_t j) {
+    auto step = [&](uint32_t j, auto any) {
       const uint32_t t = p.t0 + j;
       if (j == 0u || (t & 63u) == 0u) {
         tb = t & ~63u;
@@ -229,7 +252,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
       const bool a0 = __builtin_amdgcn_inverse_ballot_w64(w0);
       const bool a1 = __builtin_amdgcn_inverse_ballot_w64(w1);
       const h2 force = h2{a0 ? half_t(10.0) : half_t(-10.0), a1 ? half_t(10.0) : half_t(-10.0)};
-      S2 o = dynamics2(s, force, lut);
+      S2 o = dynamics2<decltype(any)::value>(s, force, lut);
       const bool d0 = v0 && done16(o.x[0], o.th[0]);
       const bool d1 = v1 && done16(o.x[1], o.th[1]);
       k[0] += d0 ? 1u : 0u;
@@ -271,10 +294,15 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
       }
       wave_done += __popcll(__ballot(d0)) + __popcll(__ballot(d1));
     };
-    uint32_t j = 0;
+    using any_angle = std::integral_constant<bool, true>;
+    using limited_angle = std::integral_constant<bool, false>;
+    // the first step (any angle), then rounds of kRefill steps (angles within
+    // the limit or NaN), each followed by the refill, then the rest
+    if (p.T > 0u) step(0u, any_angle{});
+    uint32_t j = 1;
     for (; j + kRefill <= p.T; j += kRefill) {
-#pragma unroll
-      for (uint32_t r = 0; r < kRefill; ++r) step(j + r);
+#pragma unroll 1
+      for (uint32_t r = 0; r < kRefill; ++r) step(j + r, limited_angle{});
       if (!have0) {
         draw_into(nxt, 0, p.krst, e0, k[0] + 1u);
         have0 = true;
@@ -284,7 +312,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
         have1 = true;
       }
     }
-    for (; j < p.T; ++j) step(j);
+    for (; j < p.T; ++j) step(j, limited_angle{});
     // as the one-per-lane kernel: terminations are the growth of the episode
     // index, finished returns T + len(start) - len(end)
     const bool v[2] = {v0, v1};
