@@ -82,6 +82,8 @@ def stream_bytes_per_env_step(termination_rate, T):
 # The whole-rollout kernel writing the same trajectory keeps the state in
 # registers: obs 16, reward 4, done 1 written per env-step, nothing read.
 STEP_BYTES_TRAJ_RESIDENT = 21
+# ... and in binary16: obs 8, reward 4, done 1
+STEP_BYTES_TRAJ_RESIDENT_F16 = 13
 # Algorithmic binary32 operations per environment-step of the dynamics
 # (sin, cos, 2 squares, 15 mul/add/sub/div in the accelerations, 8 in the
 # Euler update, 4 comparisons), each counted once.
@@ -201,6 +203,7 @@ def parse():
                                        "resident_1024x200", "resident_1048576x1000",
                                        "resident_f64_1048576x1000", "resident_f16_1048576x1000",
                                        "resident_traj_16777216x100",
+                                       "resident_traj_f16_16777216x100",
                                        "policy_4194304x500",
                                        "policy_separate_4194304x500",
                                        "policy_two_streams_4194304x500", "horizontal_16x4096",
@@ -472,6 +475,8 @@ def bench_configs(cp, only=None):
         res["resident_f16_1048576x1000"] = _resident_large(cp, "f16")
     if want("resident_traj_16777216x100"):
         res["resident_traj_16777216x100"] = _resident_traj(cp)
+    if want("resident_traj_f16_16777216x100"):
+        res["resident_traj_f16_16777216x100"] = _resident_traj(cp, "f16")
     if want("policy_4194304x500"):
         res["policy_4194304x500"] = _policy(cp)
     if want("policy_separate_4194304x500"):
@@ -583,23 +588,24 @@ def _resident_large(cp, precision="f32"):
     return out
 
 
-def _resident_traj(cp):
+def _resident_traj(cp, precision="f32"):
     import torch
 
     # the same 16,777,216 x 100 trajectory from the whole-rollout kernel
-    # (state in registers; the trajectory is the only HBM traffic)
+    # (state in registers; the trajectory is the only HBM traffic); in
+    # binary16 the obs planes take 2 bytes per value
     n, T = 1 << 24, 100
-    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT, precision=precision)
     cp.cp_init(s, 0)
-    tr = cp.Trajectory(n, T, stats=False, totals=False)
+    tr = cp.Trajectory(n, T, stats=False, totals=False, dtype=s.dtype)
     cp.cp_rollout(s, T, 0, tr)
     wall, ev = timed(lambda: cp.cp_rollout(s, T, 0, tr), reps=3)
     ms = ev / 3
-    gbs = STEP_BYTES_TRAJ_RESIDENT * n * T / (ms * 1e-3) / 1e9
+    bpe = STEP_BYTES_TRAJ_RESIDENT if precision == "f32" else STEP_BYTES_TRAJ_RESIDENT_F16
+    gbs = bpe * n * T / (ms * 1e-3) / 1e9
     out = {"env_steps_per_s": n * T / (ms * 1e-3), "ms": ms,
            "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": gbs / HBM_PEAK_GBS,
-                        "bytes_per_env_step": STEP_BYTES_TRAJ_RESIDENT}}
+                        "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": bpe}}
     del s, tr
     torch.cuda.empty_cache()
     return out
@@ -677,7 +683,7 @@ def _policy_separate(cp, streams):
     return {"env_steps_per_s": n * T / (ms * 1e-3), "ms": ms, "streams": streams}
 
 
-CROSSOVER_N = (1, 4, 16, 64, 256, 1024, 2048, 4096)
+CROSSOVER_N = (1, 4, 16, 64, 256, 1024, 2048, 4096, 16384, 65536)
 CROSSOVER_LEVELS = (("unfused", "CP_UNFUSED", False), ("fused", "CP_FUSED", True),
                     ("resident", "CP_RESIDENT", False))
 
