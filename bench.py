@@ -100,38 +100,34 @@ BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 # as null until the counters are taken again.
 _CSRC = "paper_2301_13062_amd/csrc/"
 COUNTERS = {
-    # HBM traffic of one headline launch (fused streaming step, 16,777,216
-    # environments writing the trajectory): FETCH_SIZE and WRITE_SIZE, KiB
-    # per dispatch (profiles/fused_step_16777216env_hbm.md)
-    "fused_step_16777216": {
+    # HBM traffic of the headline: the streaming fused step at 16,777,216
+    # environments, FETCH_SIZE and WRITE_SIZE in KiB per launch averaged over a
+    # rollout's launches (1 first, 98 middle, 1 last)
+    "stream_step_16777216": {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_device.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "0000000000000000", "fetch_kib": 188613.5, "write_kib": 435687.5,
-        "profile": "profiles/fused_step_16777216env_hbm.md"},
-    # HBM traffic of one launch-bound launch (fused step, 65,536 environments):
-    # FETCH_SIZE and WRITE_SIZE, KiB per dispatch
+        "sha256_16": "140b1d19ba323add", "fetch_kib": 157368.8, "write_kib": 392125.0, "profile": "profiles/stream_step_16777216x100_hbm.md"},
+    # HBM traffic of one launch-bound launch (graph-replayed fused step,
+    # 65,536 environments): FETCH_SIZE and WRITE_SIZE, KiB per dispatch
     "fused_step_65536": {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_device.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "cbdc6a566c9f748a", "fetch_kib": 812.0, "write_kib": 2703.0},
+        "sha256_16": "140b1d19ba323add", "fetch_kib": 813.9, "write_kib": 2702.8, "profile": "profiles/fused_step_65536env_trace_and_traffic.md"},
     # the resident rollout, 1,048,576 x 1,000: SQ_INSTS_VALU per wave-step
     "resident_1048576x1000": {
-        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
-                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "8fdcd8aed35b7edf", "valu_per_wave_step": 71.6},
-    # the same rollout stepped in binary64 and in binary16
+        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h", _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "85766c8a36c6ab83", "valu_per_wave_step": 71.6, "envs_per_wave": 64, "profile": "profiles/resident_1048576x1000_valu.md"},
+    # the same rollout stepped in binary64 and in binary16 (the binary16 kernel
+    # holds two environments per lane: 128 per wave)
     "resident_f64_1048576x1000": {
-        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
-                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "8fdcd8aed35b7edf", "valu_per_wave_step": 97.8},
+        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h", _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "85766c8a36c6ab83", "valu_per_wave_step": 97.8, "envs_per_wave": 64, "profile": "profiles/resident_1048576x1000_valu.md"},
     "resident_f16_1048576x1000": {
-        "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
-                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "8fdcd8aed35b7edf", "valu_per_wave_step": 105.9},
+        "sources": [_CSRC + "cp_resident16.hip", _CSRC + "cp_f16_table.h", _CSRC + "cp_resident.h", _CSRC + "cp_device.h", _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "d6407d7a480f48bd", "valu_per_wave_step": 103.5, "envs_per_wave": 128, "profile": "profiles/resident_1048576x1000_valu.md"},
     # the MLP-policy rollout, 4,194,304 x 500: SQ_INSTS_VALU per wave-step and
     # the matrix cores' busy share of SIMD cycles (SQ_VALU_MFMA_BUSY_CYCLES)
     "policy_4194304x500": {
-        "sources": [_CSRC + "cp_policy.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h",
-                    _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "a6e1296e5e96d224", "valu_per_wave_step": 1937.2, "mfma_busy": 0.218},
+        "sources": [_CSRC + "cp_policy.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h", _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
+        "sha256_16": "2f0339f096b44151", "valu_per_wave_step": 1681.2, "envs_per_wave": 64, "mfma_busy": 0.237, "profile": "profiles/policy_4194304x500_mfma_valu.md"},
 }
 # The same counters' reading for a plain 1 GiB copy (1 GiB read, 1 GiB
 # written): bytes per KiB counted.
@@ -183,7 +179,7 @@ def valu_issue(key, env_steps_per_s):
     c = stored_counters(key)
     if c is None:
         return None
-    per_cycle = c["valu_per_wave_step"] * env_steps_per_s / 64 / CUS / CLOCK_PEAK_HZ
+    per_cycle = c["valu_per_wave_step"] * env_steps_per_s / c["envs_per_wave"] / CUS / CLOCK_PEAK_HZ
     return {"reading": "VALU instruction issue / issue peak",
             "valu_per_wave_step": c["valu_per_wave_step"], "stored_counters": True,
             "per_cu_per_cycle": per_cycle,
@@ -838,7 +834,7 @@ def headline_line(head, K, W):
     kern_us = head["kernel_mean_us"]
     bpe = stream_bytes_per_env_step(head["termination_rate"], T)
     gbs = bpe * n / (kern_us * 1e-6) / 1e9
-    c = COUNTERS["fused_step_16777216"]
+    c = COUNTERS["stream_step_16777216"]
     return {
         "metric": METRIC,
         "value": head["env_steps_per_s"],
@@ -859,7 +855,7 @@ def headline_line(head, K, W):
                    "envs": n, "steps_per_rollout": T, "steps_per_launch": 1, "variant": "fused"},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": gbs / HBM_PEAK_GBS,
-                     "traffic": measured_traffic_bytes("fused_step_16777216"),
+                     "traffic": measured_traffic_bytes("stream_step_16777216"),
                      "traffic_stored_counters": True, "traffic_profile": c["profile"],
                      "bytes_per_env_step": bpe,
                      "termination_rate": head["termination_rate"],

@@ -33,7 +33,7 @@ def test_stale_counters_read_as_null(monkeypatch, tmp_path):
     src.write_text("// version 1\n")
     rel = os.path.relpath(src, ROOT)
     entry = {"sources": [rel], "sha256_16": bench.sources_sha([rel]),
-             "fetch_kib": 100.0, "write_kib": 50.0, "valu_per_wave_step": 64.0}
+             "fetch_kib": 100.0, "write_kib": 50.0, "valu_per_wave_step": 64.0, "envs_per_wave": 64}
     monkeypatch.setitem(bench.COUNTERS, "probe", entry)
     assert bench.measured_traffic_bytes("probe") == pytest.approx(
         1024 * (100.0 * bench.READ_FACTOR + 50.0 * bench.WRITE_FACTOR))
@@ -57,7 +57,10 @@ def test_peaks_and_algorithmic_figures():
     assert bench.POLICY_FLOPS == 2 * (4 * 64 + 64 * 64 + 64 * 2)
     json.dumps(bench.COUNTERS)  # plain data
     assert bench.HEAD_N == 1 << 24 and bench.HEAD_T == 100
-    assert bench.COUNTERS["fused_step_16777216"]["profile"].startswith("profiles/")
+    for key, c in bench.COUNTERS.items():
+        assert os.path.isfile(os.path.join(ROOT, c["profile"])), key
+    # the two-environments-per-lane binary16 kernel counts 128 environments per wave
+    assert bench.COUNTERS["resident_f16_1048576x1000"]["envs_per_wave"] == 128
 
 
 def test_headline_line_shape():
