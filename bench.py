@@ -790,7 +790,7 @@ def _host():
     return {"nproc": os.cpu_count(), "cpu_model": model}
 
 
-def cpu_baseline(stride=32, chunk=1 << 16):
+def cpu_baseline(stride=8, chunk=1 << 16):
     """The oracle on a sample of the headline workload: every stride-th of its
     16,777,216 environments (their own global indices, so each behaves as in
     the full batch) x 100 steps with the full trajectory kept, in chunks of
