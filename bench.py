@@ -599,9 +599,23 @@ def _resident_traj(cp, precision="f32"):
     ms = ev / 3
     bpe = STEP_BYTES_TRAJ_RESIDENT if precision == "f32" else STEP_BYTES_TRAJ_RESIDENT_F16
     gbs = bpe * n * T / (ms * 1e-3) / 1e9
+    # the write reference at this size: a plain fill of the same trajectory
+    # buffers (the same bytes, the same pages), timed right after
+    planes = [tr.obs, tr.reward, tr.done]
+    nbytes = sum(a.numel() * a.element_size() for a in planes)
+
+    def fill():
+        for a in planes:
+            a.fill_(0)
+
+    fill()
+    _, fev = timed(fill, reps=3)
+    fill_gbs = nbytes / (fev / 3 * 1e-3) / 1e9
     out = {"env_steps_per_s": n * T / (ms * 1e-3), "ms": ms,
            "roofline": {"bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                        "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": bpe}}
+                        "frac": gbs / HBM_PEAK_GBS, "bytes_per_env_step": bpe},
+           "fill_same_buffers": {"bytes": nbytes, "ms": fev / 3, "GB_per_s": fill_gbs,
+                                 "kernel_frac_of_fill": gbs / fill_gbs}}
     del s, tr
     torch.cuda.empty_cache()
     return out

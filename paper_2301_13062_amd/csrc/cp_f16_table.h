@@ -120,5 +120,51 @@ constexpr RecipTable make_recip_table() {
   return t;
 }
 
+// The same reciprocals keyed by the cosine: the divisor is a function of
+// the binary16 cosine alone, and every cosine of the sin/cos table (every
+// angle up to 1/4 in magnitude) is one of the 65 binary16 values 0x3BC0 ..
+// 0x3C00 (0.96875 .. 1).  Entry c - kCosFirst holds RN32(1/d(c)) with
+//   d(c) = RN16(l RN16(4/3 - RN16(RN16(mp RN16(c c)) / M)))
+// (the binary16 step's rounding of each operation; l = 1/2, mp = RN16(0.1),
+// M = RN16(mp + 1), 4/3 rounded to binary16), so a step whose angle comes
+// from the table looks the reciprocal up from its cosine directly.  The
+// binary64 evaluation rounds each operation to binary16 exactly: products
+// and differences of binary16 values are exact in binary64, and a binary64
+// quotient rounded again to binary16 is the correctly rounded binary16
+// quotient (53 >= 2 * 11 + 2).
+constexpr uint32_t kCosFirst = 0x3BC0u, kCosLast = 0x3C00u;
+constexpr uint32_t kCosEntries = kCosLast - kCosFirst + 1u;
+
+// The binary16 value nearest to v, 0 <= v < 2 (ties to even).
+constexpr double round16(double v) {
+  return v < 1.0 ? value_of(nearest_bits(v)) : 2.0 * value_of(nearest_bits(0.5 * v));
+}
+
+constexpr double den_of_cos(double c) {
+  const double mp = round16(0.1), m = round16(mp + 1.0), four3 = round16(4.0 / 3.0);
+  const double q = round16(round16(mp * round16(c * c)) / m);
+  return round16(0.5 * round16(four3 - q));
+}
+
+struct RecipByCos {
+  float v[kCosEntries];
+};
+
+constexpr RecipByCos make_recip_by_cos_table() {
+  RecipByCos t{};
+  for (uint32_t b = kCosFirst; b <= kCosLast; ++b)
+    t.v[b - kCosFirst] = static_cast<float>(1.0 / den_of_cos(value_of(b)));
+  return t;
+}
+
+// Every cosine of the sin/cos table lies in [kCosFirst, kCosLast].
+constexpr bool cosines_in_range(const Table &t) {
+  for (uint32_t b = 0; b < kEntries; ++b) {
+    const uint32_t c = t.v[b] >> 16;
+    if (c < kCosFirst || c > kCosLast) return false;
+  }
+  return true;
+}
+
 }  // namespace f16tab
 }  // namespace cp

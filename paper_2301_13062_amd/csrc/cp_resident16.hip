@@ -22,7 +22,12 @@
 //    binary16 values (0.621 .. 0.667), whose reciprocals sit in a second LDS
 //    table, and for each of them every binary16 quotient lies at least
 //    2^-22.4 (relative) from a rounding boundary, farther than RN32(1/den)
-//    is from 1/den (2^-24).
+//    is from 1/den (2^-24).  The divisor is a function of the cosine alone,
+//    so a step whose cosine comes from the table reads RN32(1/den) from a
+//    third table keyed by the cosine (65 values) instead of forming den;
+//  * the episode counters are brought up to date at the refills of the
+//    prefetched start states only, and the episode length at the end from
+//    the step of the latest termination.
 // States a step produces hold angles within the 12-degree limit or NaN, so
 // only a launch's first step can meet an angle beyond the table: it is
 // peeled off the loop, and the loop's steps read the table alone (NaN
@@ -48,10 +53,14 @@ constexpr uint32_t kEnvsPerWave = 128u;
 // The tables, evaluated at compile time.
 __device__ const f16tab::Table kSinCos16 = f16tab::make_table();
 __device__ const f16tab::RecipTable kRecipDen16 = f16tab::make_recip_table();
+__device__ const f16tab::RecipByCos kRecipCos16 = f16tab::make_recip_by_cos_table();
+static_assert(f16tab::cosines_in_range(f16tab::make_table()),
+              "a table cosine outside the range the reciprocals are keyed by");
 // LDS layout: the sin/cos entries, then one entry of two NaNs (for NaN
-// angles), then the divisor reciprocals.
+// angles), then the divisor reciprocals, then the reciprocals by cosine.
 constexpr uint32_t kNanEntry = f16tab::kEntries;
-constexpr uint32_t kLutWords = f16tab::kEntries + 1u + f16tab::kDenEntries;
+constexpr uint32_t kRecipCosWord = f16tab::kEntries + 1u + f16tab::kDenEntries;
+constexpr uint32_t kLutWords = kRecipCosWord + f16tab::kCosEntries;
 
 __device__ __forceinline__ uint32_t bits(h2 v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ h2 of_bits(uint32_t u) { return __builtin_bit_cast(h2, u); }
@@ -77,13 +86,38 @@ __device__ __forceinline__ h2 mul_round2(h2 a, float c0, float c1) {
   return of_bits(r);
 }
 
-// RN32(1/d) for a divisor of the angular acceleration (bits b of one
-// binary16 d), from the LDS table; a NaN divisor (only with a NaN angle,
-// whose numerator is NaN too) reads the last entry.
-__device__ __forceinline__ float recip(uint32_t b, const uint32_t *lut) {
-  const uint32_t k = b - f16tab::kDenFirst;  // wraps to large for b < kDenFirst
-  const uint32_t idx = k < f16tab::kDenEntries - 1u ? k : f16tab::kDenEntries - 1u;
-  return __builtin_bit_cast(float, lut[kNanEntry + 1u + idx]);
+typedef uint16_t u16x2 __attribute__((ext_vector_type(2)));
+
+// The LDS word at byte offset `off` of the table.
+__device__ __forceinline__ uint32_t lut_at(const uint32_t *lut, uint32_t off) {
+  return *reinterpret_cast<const uint32_t *>(reinterpret_cast<const char *>(lut) + off);
+}
+
+// RN32(1/d) for the divisors of the angular acceleration of both
+// environments (the binary16 d in each half of db), from the LDS table: the
+// index d - kDenFirst per half (16-bit arithmetic: wraps to large below
+// kDenFirst), clamped to the last entry, which a NaN divisor reads (only
+// with a NaN angle, whose numerator is NaN too).
+__device__ __forceinline__ void recip2(uint32_t db, const uint32_t *lut, float &r0, float &r1) {
+  u16x2 k = __builtin_bit_cast(u16x2, db) - u16x2{uint16_t(f16tab::kDenFirst), uint16_t(f16tab::kDenFirst)};
+  k = __builtin_elementwise_min(k, u16x2{uint16_t(f16tab::kDenEntries - 1u), uint16_t(f16tab::kDenEntries - 1u)});
+  const uint32_t off = __builtin_bit_cast(uint32_t, u16x2(k << uint16_t(2)));
+  constexpr uint32_t kBase = 4u * (kNanEntry + 1u);
+  r0 = __builtin_bit_cast(float, lut_at(lut, kBase + (off & 0xFFFFu)));
+  r1 = __builtin_bit_cast(float, lut_at(lut, kBase + (off >> 16)));
+}
+
+// The same reciprocals from the cosines of both environments (cb: the
+// binary16 cosines, from the sin/cos table), clamped to the last entry,
+// which a NaN cosine reads (only with a NaN angle, whose numerator is NaN).
+__device__ __forceinline__ void recip2_by_cos(uint32_t cb, const uint32_t *lut, float &r0,
+                                              float &r1) {
+  u16x2 k = __builtin_bit_cast(u16x2, cb) - u16x2{uint16_t(f16tab::kCosFirst), uint16_t(f16tab::kCosFirst)};
+  k = __builtin_elementwise_min(k, u16x2{uint16_t(f16tab::kCosEntries - 1u), uint16_t(f16tab::kCosEntries - 1u)});
+  const uint32_t off = __builtin_bit_cast(uint32_t, u16x2(k << uint16_t(2)));
+  constexpr uint32_t kBase = 4u * kRecipCosWord;
+  r0 = __builtin_bit_cast(float, lut_at(lut, kBase + (off & 0xFFFFu)));
+  r1 = __builtin_bit_cast(float, lut_at(lut, kBase + (off >> 16)));
 }
 
 struct S2 {
@@ -115,9 +149,18 @@ __device__ __forceinline__ void sincos2(h2 th, const uint32_t *lut, h2 &sn, h2 &
   const uint32_t a0 = t & 0x7FFFu, a1 = (t >> 16) & 0x7FFFu;
   uint32_t e0, e1;
   if (!kAny) {
-    e0 = lut[a0 <= f16tab::kLast ? a0 : kNanEntry] ^ (t & 0x8000u);  // the sign of sin(-x)
-    e1 = lut[a1 <= f16tab::kLast ? a1 : kNanEntry] ^ ((t >> 16) & 0x8000u);
-  } else if (__all(a0 <= f16tab::kLast && a1 <= f16tab::kLast)) {
+    // both table offsets at once: |angle| bits per half, clamped to the
+    // entry of NaNs (every angle above 1/4 here is a NaN), times 4
+    u16x2 a = __builtin_bit_cast(u16x2, t & 0x7FFF7FFFu);
+    a = __builtin_elementwise_min(a, u16x2{uint16_t(kNanEntry), uint16_t(kNanEntry)});
+    const uint32_t off = __builtin_bit_cast(uint32_t, u16x2(a << uint16_t(2)));
+    e0 = lut_at(lut, off & 0xFFFFu);
+    e1 = lut_at(lut, off >> 16);
+    sn = of_bits(__builtin_amdgcn_perm(e1, e0, 0x05040100u) ^ (t & 0x80008000u));  // sin(-x) = -sin(x)
+    c = of_bits(__builtin_amdgcn_perm(e1, e0, 0x07060302u));
+    return;
+  }
+  if (__all(a0 <= f16tab::kLast && a1 <= f16tab::kLast)) {
     e0 = lut[a0] ^ (t & 0x8000u);
     e1 = lut[a1] ^ ((t >> 16) & 0x8000u);
   } else {
@@ -140,12 +183,19 @@ __device__ __forceinline__ S2 dynamics2(const S2 &s, h2 force, const uint32_t *l
   h2 sn, c;
   sincos2<kAny>(s.th, lut, sn, c);
   const h2 thd2 = s.thd * s.thd;
-  const h2 c2 = c * c;
   const h2 temp = mul_round2(force + pml * thd2 * sn, kInvTotalMass16);
   const h2 num = g * sn - c * temp;
-  const h2 den = l * (four3 - mul_round2(mp * c2, kInvTotalMass16));
-  const uint32_t db = bits(den);
-  const h2 thacc = mul_round2(num, recip(db & 0xFFFFu, lut), recip(db >> 16, lut));
+  float r0, r1;
+  if (kAny) {
+    // any cosine: the divisor formed, its reciprocal looked up
+    const h2 c2 = c * c;
+    const h2 den = l * (four3 - mul_round2(mp * c2, kInvTotalMass16));
+    recip2(bits(den), lut, r0, r1);
+  } else {
+    // a cosine from the table (or NaN): the reciprocal by the cosine
+    recip2_by_cos(bits(c), lut, r0, r1);
+  }
+  const h2 thacc = mul_round2(num, r0, r1);
   const h2 xacc = temp - mul_round2(pml * thacc * c, kInvTotalMass16);
   return S2{s.x + tau * s.xd, s.xd + tau * xacc, s.th + tau * s.thd, s.thd + tau * thacc};
 }
@@ -155,13 +205,24 @@ __device__ __forceinline__ bool done16(half_t x, half_t th) {
   return x < -xl || x > xl || th < -tl || th > tl;
 }
 
-// Start state of episode k of env into half `h` of the planes of n.
-__device__ __forceinline__ void draw_into(S2 &n, int h, U2 key, uint32_t env, uint32_t k) {
+// Prefetched start states of both environments, kept packed (x, x_dot,
+// theta, theta_dot: one word each, environment 0 in the low half).
+struct W4 {
+  uint32_t x, xd, th, thd;
+};
+
+__device__ __forceinline__ uint32_t put16(uint32_t w, int h, half_t v) {
+  const uint32_t b = __builtin_bit_cast(uint16_t, v);
+  return h == 0 ? (w & 0xFFFF0000u) | b : (w & 0x0000FFFFu) | (b << 16);
+}
+
+// Start state of episode k of env into half `h` of n.
+__device__ __forceinline__ void draw_into(W4 &n, int h, U2 key, uint32_t env, uint32_t k) {
   const State16 d = PrecF16::draw(key, env, k);
-  n.x[h] = d.x;
-  n.xd[h] = d.xd;
-  n.th[h] = d.th;
-  n.thd[h] = d.thd;
+  n.x = put16(n.x, h, d.x);
+  n.xd = put16(n.xd, h, d.xd);
+  n.th = put16(n.th, h, d.th);
+  n.thd = put16(n.thd, h, d.thd);
 }
 
 // The same draw out of line, for a second termination before the refill
@@ -176,16 +237,16 @@ __device__ __attribute__((noinline)) uint64_t draw_late(U2 key, uint32_t env, ui
   return (static_cast<uint64_t>(w1) << 32) | w0;
 }
 
-__device__ __forceinline__ void put_late(S2 &n, int h, uint64_t w) {
-  n.x[h] = __builtin_bit_cast(half_t, uint16_t(w));
-  n.xd[h] = __builtin_bit_cast(half_t, uint16_t(w >> 16));
-  n.th[h] = __builtin_bit_cast(half_t, uint16_t(w >> 32));
-  n.thd[h] = __builtin_bit_cast(half_t, uint16_t(w >> 48));
+__device__ __forceinline__ void put_late(W4 &n, int h, uint64_t w) {
+  n.x = put16(n.x, h, __builtin_bit_cast(half_t, uint16_t(w)));
+  n.xd = put16(n.xd, h, __builtin_bit_cast(half_t, uint16_t(w >> 16)));
+  n.th = put16(n.th, h, __builtin_bit_cast(half_t, uint16_t(w >> 32)));
+  n.thd = put16(n.thd, h, __builtin_bit_cast(half_t, uint16_t(w >> 48)));
 }
 
-// Per-half select: the planes of r where m (0xFFFF per half) is set.
-__device__ __forceinline__ h2 pick(uint32_t m, h2 r, h2 v) {
-  return of_bits((bits(r) & m) | (bits(v) & ~m));
+// Per-half select: the halves of r where m (0xFFFF per half) is set.
+__device__ __forceinline__ h2 pick(uint32_t m, uint32_t r, h2 v) {
+  return of_bits((r & m) | (bits(v) & ~m));
 }
 
 template <bool kTraj>
@@ -194,7 +255,8 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
   for (uint32_t b = threadIdx.x; b < kLutWords; b += kBlock16)
     lut[b] = b < f16tab::kEntries ? kSinCos16.v[b]
              : b == kNanEntry     ? 0x7E007E00u
-                                  : __builtin_bit_cast(uint32_t, kRecipDen16.v[b - kNanEntry - 1u]);
+             : b < kRecipCosWord  ? __builtin_bit_cast(uint32_t, kRecipDen16.v[b - kNanEntry - 1u])
+                                  : __builtin_bit_cast(uint32_t, kRecipCos16.v[b - kRecipCosWord]);
   __syncthreads();
 
   const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
@@ -207,8 +269,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
   half_t *const pthd = reinterpret_cast<half_t *>(p.thd);
   half_t *const pobs = reinterpret_cast<half_t *>(p.obs);
   const uint32_t e0 = p.env_base + i0, e1 = p.env_base + i1;
-  unsigned long long wave_done = 0u;
-  uint32_t returns = 0u;
+  uint32_t n_done_lane = 0u, returns = 0u;
   // Waves wholly past the batch skip the loop (they still take part in the
   // block's final reduction).
   if (base < p.n) {
@@ -224,9 +285,13 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
       k0[1] = p.ep_index[i1];
       len0[1] = p.ep_len[i1];
     }
-    uint32_t k[2] = {k0[0], k0[1]}, len[2] = {len0[0], len0[1]};
+    // Episode counters are brought up to date at the refills only: while
+    // have[h] holds, environment h is in episode k[h]; after a termination
+    // that used the prefetched start state (have[h] false) it is in episode
+    // k[h] + 1.  last[h]: the step (of this launch) of the latest termination.
+    uint32_t k[2] = {k0[0], k0[1]}, last[2] = {0u, 0u};
     // next start states, drawn ahead of time; have[h]: drawn for half h
-    S2 nxt;
+    W4 nxt{0u, 0u, 0u, 0u};
     draw_into(nxt, 0, p.krst, e0, k[0] + 1u);
     draw_into(nxt, 1, p.krst, e1, k[1] + 1u);
     bool have0 = true, have1 = true;
@@ -255,13 +320,18 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
       S2 o = dynamics2<decltype(any)::value>(s, force, lut);
       const bool d0 = v0 && done16(o.x[0], o.th[0]);
       const bool d1 = v1 && done16(o.x[1], o.th[1]);
-      k[0] += d0 ? 1u : 0u;
-      k[1] += d1 ? 1u : 0u;
-      len[0] = d0 ? 0u : len[0] + 1u;
-      len[1] = d1 ? 0u : len[1] + 1u;
-      // a second termination before the refill draws its start state now
-      if (d0 && !have0) put_late(nxt, 0, draw_late(p.krst, e0, k[0]));
-      if (d1 && !have1) put_late(nxt, 1, draw_late(p.krst, e1, k[1]));
+      last[0] = d0 ? j : last[0];
+      last[1] = d1 ? j : last[1];
+      // a second termination before the refill: the episode that began at
+      // the first one is counted now, and the next start state drawn now
+      if (d0 && !have0) {
+        k[0] += 1u;
+        put_late(nxt, 0, draw_late(p.krst, e0, k[0] + 1u));
+      }
+      if (d1 && !have1) {
+        k[1] += 1u;
+        put_late(nxt, 1, draw_late(p.krst, e1, k[1] + 1u));
+      }
       const uint32_t m = (d0 ? 0x0000FFFFu : 0u) | (d1 ? 0xFFFF0000u : 0u);
       o.x = pick(m, nxt.x, o.x);
       o.xd = pick(m, nxt.xd, o.xd);
@@ -292,7 +362,6 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
           if (v1) p.done[plane + i1] = uint8_t(d1);
         }
       }
-      wave_done += __popcll(__ballot(d0)) + __popcll(__ballot(d1));
     };
     using any_angle = std::integral_constant<bool, true>;
     using limited_angle = std::integral_constant<bool, false>;
@@ -304,15 +373,24 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
 #pragma unroll 1
       for (uint32_t r = 0; r < kRefill; ++r) step(j + r, limited_angle{});
       if (!have0) {
+        k[0] += 1u;
         draw_into(nxt, 0, p.krst, e0, k[0] + 1u);
         have0 = true;
       }
       if (!have1) {
+        k[1] += 1u;
         draw_into(nxt, 1, p.krst, e1, k[1] + 1u);
         have1 = true;
       }
     }
     for (; j < p.T; ++j) step(j, limited_angle{});
+    if (!have0) k[0] += 1u;
+    if (!have1) k[1] += 1u;
+    // the episode length at the end: the steps since the latest termination,
+    // or the starting length plus T without one
+    uint32_t len[2];
+#pragma unroll
+    for (int h = 0; h < 2; ++h) len[h] = k[h] != k0[h] ? p.T - 1u - last[h] : len0[h] + p.T;
     // as the one-per-lane kernel: terminations are the growth of the episode
     // index, finished returns T + len(start) - len(end)
     const bool v[2] = {v0, v1};
@@ -322,6 +400,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
       if (!v[h]) continue;
       const uint32_t i = ii[h];
       const uint32_t n_done = k[h] - k0[h], ret = p.T + len0[h] - len[h];
+      n_done_lane += n_done;
       returns += ret;
       px[i] = s.x[h];
       pxd[i] = s.xd[h];
@@ -338,7 +417,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
       if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + ret;
     }
   }
-  if (p.global) block_publish<kBlock16>(p.global, wave_done, returns, true);
+  if (p.global) block_publish<kBlock16>(p.global, n_done_lane, returns, false);
 }
 
 }  // namespace

@@ -21,8 +21,10 @@ def test_every_entry_is_the_rounded_sin_and_cos(tmp_path):
                    check=True, capture_output=True)
     out = subprocess.run([str(exe)], check=True, capture_output=True, text=True).stdout.split()
     vals = np.array([int(v, 16) for v in out], dtype=np.uint64)
-    tab, rec = vals[:0x3401], vals[0x3401:]
-    assert len(rec) == 0x3955 - 0x38F8 + 1  # bit patterns 0 .. 0x3400 (= 0.25), then 94 divisors
+    n_den = 0x3955 - 0x38F8 + 1
+    tab, rec, rec_c = vals[:0x3401], vals[0x3401:0x3401 + n_den], vals[0x3401 + n_den:]
+    # bit patterns 0 .. 0x3400 (= 0.25), then 94 divisors, then 65 cosines
+    assert len(rec) == n_den and len(rec_c) == 0x3C00 - 0x3BC0 + 1
     x = np.arange(len(tab), dtype=np.uint16).view(np.float16).astype(np.float64)
     assert x[-1] == 0.25 and x[1] == 2.0 ** -24
     sin16 = np.array([np.float16(math.sin(v)) for v in x]).view(np.uint16)
@@ -33,14 +35,30 @@ def test_every_entry_is_the_rounded_sin_and_cos(tmp_path):
     # exact rationals
     from fractions import Fraction
 
-    for k, r in enumerate(rec):
-        d = Fraction(float(np.uint16(0x38F8 + k).view(np.float16)))
+    def nearest32(r, d):
         got = Fraction(float(np.uint32(r).view(np.float32)))
         e = got.numerator.bit_length() - got.denominator.bit_length()
         if got < Fraction(2) ** e:
             e -= 1  # now 2^e <= got < 2^(e + 1)
         ulp = Fraction(2) ** (e - 23)
-        assert abs(got - 1 / d) <= ulp / 2, k
+        return abs(got - 1 / d) <= ulp / 2
+
+    for k, r in enumerate(rec):
+        assert nearest32(r, Fraction(float(np.uint16(0x38F8 + k).view(np.float16)))), k
+    # keyed by the cosine: every table cosine is in 0x3BC0 .. 0x3C00, and
+    # entry c holds RN32(1 / d(c)), d(c) rounded as the binary16 step rounds
+    # it (numpy binary16 rounding of each binary64 operation)
+    assert (tab >> 16).min() == 0x3BC0 and (tab >> 16).max() == 0x3C00
+
+    def f16(v):
+        return float(np.float16(v))
+
+    mp, four3 = f16(0.1), f16(4.0 / 3.0)
+    m = f16(mp + 1.0)
+    for k, r in enumerate(rec_c):
+        c = float(np.uint16(0x3BC0 + k).view(np.float16))
+        d = f16(0.5 * f16(four3 - f16(f16(mp * f16(c * c)) / m)))
+        assert nearest32(r, Fraction(d)), k
 
 
 def test_the_divisors_are_every_one_the_step_can_form():
