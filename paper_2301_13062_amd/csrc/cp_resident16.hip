@@ -225,6 +225,32 @@ __device__ __forceinline__ void draw_into(W4 &n, int h, U2 key, uint32_t env, ui
   n.thd = put16(n.thd, h, d.thd);
 }
 
+// The start state of episode k of env as two words of binary16 pairs:
+// (x, x_dot) and (theta, theta_dot).
+__device__ __forceinline__ void draw_words(U2 key, uint32_t env, uint32_t k, uint32_t &w0,
+                                           uint32_t &w1) {
+  const State16 d = PrecF16::draw(key, env, k);
+  w0 = uint32_t(__builtin_bit_cast(uint16_t, d.x)) |
+       (uint32_t(__builtin_bit_cast(uint16_t, d.xd)) << 16);
+  w1 = uint32_t(__builtin_bit_cast(uint16_t, d.th)) |
+       (uint32_t(__builtin_bit_cast(uint16_t, d.thd)) << 16);
+}
+
+// Half h of n from the words of draw_words.
+__device__ __forceinline__ void put_words(W4 &n, int h, uint32_t w0, uint32_t w1) {
+  if (h == 0) {
+    n.x = __builtin_amdgcn_perm(n.x, w0, 0x07060100u);   // high half kept, low from w0.lo
+    n.xd = __builtin_amdgcn_perm(n.xd, w0, 0x07060302u);  // low from w0.hi
+    n.th = __builtin_amdgcn_perm(n.th, w1, 0x07060100u);
+    n.thd = __builtin_amdgcn_perm(n.thd, w1, 0x07060302u);
+  } else {
+    n.x = __builtin_amdgcn_perm(w0, n.x, 0x05040100u);    // high from w0.lo, low kept
+    n.xd = __builtin_amdgcn_perm(w0, n.xd, 0x07060100u);  // high from w0.hi
+    n.th = __builtin_amdgcn_perm(w1, n.th, 0x05040100u);
+    n.thd = __builtin_amdgcn_perm(w1, n.thd, 0x07060100u);
+  }
+}
+
 // The same draw out of line, for a second termination before the refill
 // (never, for episodes started from the reset distribution, which last at
 // least 8 steps): x, x_dot in the first word, theta, theta_dot in the second.
@@ -244,6 +270,10 @@ __device__ __forceinline__ void put_late(W4 &n, int h, uint64_t w) {
   n.thd = put16(n.thd, h, __builtin_bit_cast(half_t, uint16_t(w >> 48)));
 }
 
+// Keeps the compiler from moving memory accesses across this point (LDS
+// exchanges within one wave, whose accesses the LDS executes in order).
+__device__ __forceinline__ void lds_order() { asm volatile("" ::: "memory"); }
+
 // Per-half select: the halves of r where m (0xFFFF per half) is set.
 __device__ __forceinline__ h2 pick(uint32_t m, uint32_t r, h2 v) {
   return of_bits((r & m) | (bits(v) & ~m));
@@ -252,6 +282,7 @@ __device__ __forceinline__ h2 pick(uint32_t m, uint32_t r, h2 v) {
 template <bool kTraj>
 __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
   __shared__ uint32_t lut[kLutWords];
+  __shared__ uint32_t xch[kWaves16][64][2];  // each wave's refill exchange
   for (uint32_t b = threadIdx.x; b < kLutWords; b += kBlock16)
     lut[b] = b < f16tab::kEntries ? kSinCos16.v[b]
              : b == kNanEntry     ? 0x7E007E00u
@@ -288,8 +319,9 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
     // Episode counters are brought up to date at the refills only: while
     // have[h] holds, environment h is in episode k[h]; after a termination
     // that used the prefetched start state (have[h] false) it is in episode
-    // k[h] + 1.  last[h]: the step (of this launch) of the latest termination.
-    uint32_t k[2] = {k0[0], k0[1]}, last[2] = {0u, 0u};
+    // k[h] + 1.  last: the step (of this launch, below 2^16) of the latest
+    // termination of each environment, in the halves of one word.
+    uint32_t k[2] = {k0[0], k0[1]}, last = 0u;
     // next start states, drawn ahead of time; have[h]: drawn for half h
     W4 nxt{0u, 0u, 0u, 0u};
     draw_into(nxt, 0, p.krst, e0, k[0] + 1u);
@@ -320,8 +352,6 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
       S2 o = dynamics2<decltype(any)::value>(s, force, lut);
       const bool d0 = v0 && done16(o.x[0], o.th[0]);
       const bool d1 = v1 && done16(o.x[1], o.th[1]);
-      last[0] = d0 ? j : last[0];
-      last[1] = d1 ? j : last[1];
       // a second termination before the refill: the episode that began at
       // the first one is counted now, and the next start state drawn now
       if (d0 && !have0) {
@@ -333,6 +363,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
         put_late(nxt, 1, draw_late(p.krst, e1, k[1] + 1u));
       }
       const uint32_t m = (d0 ? 0x0000FFFFu : 0u) | (d1 ? 0xFFFF0000u : 0u);
+      last = (last & ~m) | (j * 0x00010001u & m);
       o.x = pick(m, nxt.x, o.x);
       o.xd = pick(m, nxt.xd, o.xd);
       o.th = pick(m, nxt.th, o.th);
@@ -363,6 +394,47 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
         }
       }
     };
+    // The refill after a round: the environments that used their prefetched
+    // start state (about a third of them after 8 steps) get the next one.
+    // Their requests (environment, episode) are packed into consecutive
+    // slots of the wave's exchange area in LDS, lane r of the wave draws
+    // request r -- one generator pass for up to 64 requests, instead of one
+    // pass for each half whenever any of its lanes asks -- and the
+    // requesting lanes read their start states back.  The slots of a wave are
+    // its own and the LDS executes a wave's accesses in program order, so
+    // only the compiler's ordering needs fixing (lds_order).
+    auto refill = [&]() {
+      const unsigned long long m0 = __ballot(!have0), m1 = __ballot(!have1);
+      if ((m0 | m1) == 0u) return;
+      const uint32_t c0 = uint32_t(__popcll(m0)), total = c0 + uint32_t(__popcll(m1));
+      const uint32_t s0 = __builtin_amdgcn_mbcnt_hi(uint32_t(m0 >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m0), 0u));
+      const uint32_t s1 = c0 + __builtin_amdgcn_mbcnt_hi(uint32_t(m1 >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m1), 0u));
+      if (!have0) k[0] += 1u;
+      if (!have1) k[1] += 1u;
+      uint32_t(*const slot)[2] = xch[wave];
+      for (uint32_t base = 0; base < total; base += 64u) {
+        if (!have0 && s0 - base < 64u) {
+          slot[s0 - base][0] = e0;
+          slot[s0 - base][1] = k[0] + 1u;
+        }
+        if (!have1 && s1 - base < 64u) {
+          slot[s1 - base][0] = e1;
+          slot[s1 - base][1] = k[1] + 1u;
+        }
+        lds_order();
+        uint32_t w0 = 0u, w1 = 0u;
+        if (base + lane < total) draw_words(p.krst, slot[lane][0], slot[lane][1], w0, w1);
+        lds_order();
+        slot[lane][0] = w0;
+        slot[lane][1] = w1;
+        lds_order();
+        if (!have0 && s0 - base < 64u) put_words(nxt, 0, slot[s0 - base][0], slot[s0 - base][1]);
+        if (!have1 && s1 - base < 64u) put_words(nxt, 1, slot[s1 - base][0], slot[s1 - base][1]);
+        lds_order();
+      }
+      have0 = true;
+      have1 = true;
+    };
     using any_angle = std::integral_constant<bool, true>;
     using limited_angle = std::integral_constant<bool, false>;
     // the first step (any angle), then rounds of kRefill steps (angles within
@@ -372,16 +444,7 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
     for (; j + kRefill <= p.T; j += kRefill) {
 #pragma unroll 1
       for (uint32_t r = 0; r < kRefill; ++r) step(j + r, limited_angle{});
-      if (!have0) {
-        k[0] += 1u;
-        draw_into(nxt, 0, p.krst, e0, k[0] + 1u);
-        have0 = true;
-      }
-      if (!have1) {
-        k[1] += 1u;
-        draw_into(nxt, 1, p.krst, e1, k[1] + 1u);
-        have1 = true;
-      }
+      refill();
     }
     for (; j < p.T; ++j) step(j, limited_angle{});
     if (!have0) k[0] += 1u;
@@ -390,7 +453,10 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
     // or the starting length plus T without one
     uint32_t len[2];
 #pragma unroll
-    for (int h = 0; h < 2; ++h) len[h] = k[h] != k0[h] ? p.T - 1u - last[h] : len0[h] + p.T;
+    for (int h = 0; h < 2; ++h) {
+      const uint32_t l = h == 0 ? last & 0xFFFFu : last >> 16;
+      len[h] = k[h] != k0[h] ? p.T - 1u - l : len0[h] + p.T;
+    }
     // as the one-per-lane kernel: terminations are the growth of the episode
     // index, finished returns T + len(start) - len(end)
     const bool v[2] = {v0, v1};
@@ -424,15 +490,32 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
 
 bool resident_f16x2_applies(const RolloutParams &p) { return p.env_base % 64u == 0u; }
 
+// At most 2^16 steps per launch (the kernel keeps step indices in 16-bit
+// halves); a longer rollout is split into launches the way steps_per_launch
+// splits one, which changes no result.
+constexpr uint32_t kMaxStepsF16x2 = 1u << 16;
+
 hipError_t launch_resident_f16x2(const RolloutParams &p, hipStream_t stream) {
   const uint32_t per_block = kBlock16 * 2u;
   const dim3 grid((p.n + per_block - 1u) / per_block);
   const bool traj = p.obs || p.reward || p.done;
-  if (traj)
-    hipLaunchKernelGGL(k_resident_f16x2<true>, grid, dim3(kBlock16), 0, stream, p);
-  else
-    hipLaunchKernelGGL(k_resident_f16x2<false>, grid, dim3(kBlock16), 0, stream, p);
-  return hipGetLastError();
+  for (uint64_t j = 0; j < p.T || j == 0u; j += kMaxStepsF16x2) {
+    RolloutParams q = p;
+    q.t0 = p.t0 + uint32_t(j);
+    q.T = uint32_t(p.T - j < kMaxStepsF16x2 ? p.T - j : kMaxStepsF16x2);
+    q.first = p.first && j == 0u;
+    // trajectory rows: 4 * n binary16 obs values, n rewards, n flags per step
+    if (p.obs) q.obs = reinterpret_cast<float *>(reinterpret_cast<half_t *>(p.obs) + size_t(j) * 4u * p.n);
+    if (p.reward) q.reward = p.reward + size_t(j) * p.n;
+    if (p.done) q.done = p.done + size_t(j) * p.n;
+    if (traj)
+      hipLaunchKernelGGL(k_resident_f16x2<true>, grid, dim3(kBlock16), 0, stream, q);
+    else
+      hipLaunchKernelGGL(k_resident_f16x2<false>, grid, dim3(kBlock16), 0, stream, q);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess || p.T == 0u) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace cp

@@ -259,3 +259,27 @@ def test_f16_wide_states_both_kernel_forms(gpu, env_base):
         for f in ("done_count", "ret_sum"):
             assert np.array_equal(getattr(tr, f).cpu().numpy().view(np.uint32), out[f]), f
         assert int(tr.totals[0]) == int(out["done_count"].sum())
+
+
+def test_f16_rollout_longer_than_one_launch(gpu):
+    # the two-environments-per-lane binary16 kernel keeps step indices in
+    # 16-bit halves and splits a rollout into launches of at most 2^16 steps:
+    # a rollout across that boundary (with the done flags of the steps around
+    # it) equals the oracle's, counters, statistics and totals included
+    n, T = 192, (1 << 16) + 300
+    s = handle(n, "f16")
+    cp.cp_init(s, 3)
+    tr = traj(n, T, "f16", obs=False, reward=False)
+    cp.cp_rollout(s, T, 4, tr)
+    torch.cuda.synchronize()
+    o = oracle_state(n, "f16")
+    O.init_prec(o, 3)
+    out = O.rollout_prec(o, T, act_seed=4, traj=("done",))
+    g, gk, gl = gpu_state(s)
+    assert np.array_equal(tr.done.cpu().numpy(), out["done"])
+    assert _f16_equal(g, o.state())
+    assert np.array_equal(gk, o.ep_index) and np.array_equal(gl, o.ep_len)
+    for f in ("done_count", "ret_sum"):
+        assert np.array_equal(getattr(tr, f).cpu().numpy().view(np.uint32), out[f]), f
+    tot = tr.totals.cpu().numpy()
+    assert tot[0] == out["done_count"].sum() and tot[1] == out["ret_sum"].sum()
