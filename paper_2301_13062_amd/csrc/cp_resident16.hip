@@ -31,7 +31,7 @@
 // States a step produces hold angles within the 12-degree limit or NaN, so
 // only a launch's first step can meet an angle beyond the table: it is
 // peeled off the loop, and the loop's steps read the table alone (NaN
-// angles reading an entry of NaNs).
+// angles reading entries of NaNs).
 // The actions of a wave's 128 environments are two 64-environment blocks of
 // the random stream, each a lane mask (one select per environment).
 #include <type_traits>
@@ -56,11 +56,18 @@ __device__ const f16tab::RecipTable kRecipDen16 = f16tab::make_recip_table();
 __device__ const f16tab::RecipByCos kRecipCos16 = f16tab::make_recip_by_cos_table();
 static_assert(f16tab::cosines_in_range(f16tab::make_table()),
               "a table cosine outside the range the reciprocals are keyed by");
-// LDS layout: the sin/cos entries, then one entry of two NaNs (for NaN
-// angles), then the divisor reciprocals, then the reciprocals by cosine.
-constexpr uint32_t kNanEntry = f16tab::kEntries;
-constexpr uint32_t kRecipCosWord = f16tab::kEntries + 1u + f16tab::kDenEntries;
-constexpr uint32_t kLutWords = kRecipCosWord + f16tab::kCosEntries;
+// LDS layout: the divisor reciprocals, the reciprocals by cosine, then the
+// sin/cos entries followed by entries of two NaNs (for NaN angles).
+// The angle part spans every 14-bit pattern (|angle| bits & 0x3FFF), entries
+// past 1/4 holding two NaNs: an angle within the limit indexes its own
+// entry and a NaN angle (bits 0x7C01 .. 0x7FFF) one of the NaN entries.
+// The two small tables come first, so that every table's byte offset fits
+// the immediate offset of an LDS read.
+constexpr uint32_t kAngleWords = 1u << 14;
+constexpr uint32_t kDenWord = 0u;
+constexpr uint32_t kRecipCosWord = kDenWord + f16tab::kDenEntries;
+constexpr uint32_t kAngleWord = kRecipCosWord + f16tab::kCosEntries;
+constexpr uint32_t kLutWords = kAngleWord + kAngleWords;
 
 __device__ __forceinline__ uint32_t bits(h2 v) { return __builtin_bit_cast(uint32_t, v); }
 __device__ __forceinline__ h2 of_bits(uint32_t u) { return __builtin_bit_cast(h2, u); }
@@ -102,22 +109,25 @@ __device__ __forceinline__ void recip2(uint32_t db, const uint32_t *lut, float &
   u16x2 k = __builtin_bit_cast(u16x2, db) - u16x2{uint16_t(f16tab::kDenFirst), uint16_t(f16tab::kDenFirst)};
   k = __builtin_elementwise_min(k, u16x2{uint16_t(f16tab::kDenEntries - 1u), uint16_t(f16tab::kDenEntries - 1u)});
   const uint32_t off = __builtin_bit_cast(uint32_t, u16x2(k << uint16_t(2)));
-  constexpr uint32_t kBase = 4u * (kNanEntry + 1u);
+  constexpr uint32_t kBase = 4u * kDenWord;
   r0 = __builtin_bit_cast(float, lut_at(lut, kBase + (off & 0xFFFFu)));
   r1 = __builtin_bit_cast(float, lut_at(lut, kBase + (off >> 16)));
 }
 
 // The same reciprocals from the cosines of both environments (cb: the
-// binary16 cosines, from the sin/cos table), clamped to the last entry,
-// which a NaN cosine reads (only with a NaN angle, whose numerator is NaN).
+// binary16 cosines of the sin/cos table, each one of the 65 keys, or the NaN
+// 0x7E00 of a NaN entry): byte offset (c - kCosFirst) * 4 mod 2^16, of which
+// the low 9 bits are kept -- the keys' own offsets 0 .. 256, and for the NaN
+// cosine 0x900 -> 0x100, the last key's entry, whose value does not matter
+// there (that angle's numerator is NaN too).
 __device__ __forceinline__ void recip2_by_cos(uint32_t cb, const uint32_t *lut, float &r0,
                                               float &r1) {
-  u16x2 k = __builtin_bit_cast(u16x2, cb) - u16x2{uint16_t(f16tab::kCosFirst), uint16_t(f16tab::kCosFirst)};
-  k = __builtin_elementwise_min(k, u16x2{uint16_t(f16tab::kCosEntries - 1u), uint16_t(f16tab::kCosEntries - 1u)});
-  const uint32_t off = __builtin_bit_cast(uint32_t, u16x2(k << uint16_t(2)));
+  constexpr uint16_t kFirst4 = uint16_t(f16tab::kCosFirst << 2);
+  const uint32_t off = __builtin_bit_cast(
+      uint32_t, u16x2(u16x2(__builtin_bit_cast(u16x2, cb) << uint16_t(2)) - u16x2{kFirst4, kFirst4}));
   constexpr uint32_t kBase = 4u * kRecipCosWord;
-  r0 = __builtin_bit_cast(float, lut_at(lut, kBase + (off & 0xFFFFu)));
-  r1 = __builtin_bit_cast(float, lut_at(lut, kBase + (off >> 16)));
+  r0 = __builtin_bit_cast(float, lut_at(lut, kBase + (off & 0x1FFu)));
+  r1 = __builtin_bit_cast(float, lut_at(lut, kBase + ((off >> 16) & 0x1FFu)));
 }
 
 struct S2 {
@@ -142,27 +152,26 @@ __device__ __attribute__((noinline)) uint64_t sincos2_beyond(uint32_t t) {
 // sin and cos of both angles of th.  kAny: any angle (a launch's first
 // step): from the table when every lane's angles are at most 1/4 in
 // magnitude, else for the whole wave out of line.  Otherwise the angle is
-// within the limit or NaN: the table alone, NaN reading the entry of NaNs.
+// within the limit or NaN: the table alone, NaN reading an entry of NaNs.
 template <bool kAny>
 __device__ __forceinline__ void sincos2(h2 th, const uint32_t *lut, h2 &sn, h2 &c) {
   const uint32_t t = bits(th);
   const uint32_t a0 = t & 0x7FFFu, a1 = (t >> 16) & 0x7FFFu;
   uint32_t e0, e1;
   if (!kAny) {
-    // both table offsets at once: |angle| bits per half, clamped to the
-    // entry of NaNs (every angle above 1/4 here is a NaN), times 4
-    u16x2 a = __builtin_bit_cast(u16x2, t & 0x7FFF7FFFu);
-    a = __builtin_elementwise_min(a, u16x2{uint16_t(kNanEntry), uint16_t(kNanEntry)});
+    // both table offsets at once: the low 14 bits of each angle (an angle
+    // within the limit is below 2^14, a NaN lands on a NaN entry), times 4
+    const u16x2 a = __builtin_bit_cast(u16x2, t & 0x3FFF3FFFu);
     const uint32_t off = __builtin_bit_cast(uint32_t, u16x2(a << uint16_t(2)));
-    e0 = lut_at(lut, off & 0xFFFFu);
-    e1 = lut_at(lut, off >> 16);
+    e0 = lut_at(lut, 4u * kAngleWord + (off & 0xFFFFu));
+    e1 = lut_at(lut, 4u * kAngleWord + (off >> 16));
     sn = of_bits(__builtin_amdgcn_perm(e1, e0, 0x05040100u) ^ (t & 0x80008000u));  // sin(-x) = -sin(x)
     c = of_bits(__builtin_amdgcn_perm(e1, e0, 0x07060302u));
     return;
   }
   if (__all(a0 <= f16tab::kLast && a1 <= f16tab::kLast)) {
-    e0 = lut[a0] ^ (t & 0x8000u);
-    e1 = lut[a1] ^ ((t >> 16) & 0x8000u);
+    e0 = lut[kAngleWord + a0] ^ (t & 0x8000u);
+    e1 = lut[kAngleWord + a1] ^ ((t >> 16) & 0x8000u);
   } else {
     const uint64_t e = sincos2_beyond(t);
     e0 = uint32_t(e);
@@ -284,10 +293,10 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
   __shared__ uint32_t lut[kLutWords];
   __shared__ uint32_t xch[kWaves16][64][2];  // each wave's refill exchange
   for (uint32_t b = threadIdx.x; b < kLutWords; b += kBlock16)
-    lut[b] = b < f16tab::kEntries ? kSinCos16.v[b]
-             : b == kNanEntry     ? 0x7E007E00u
-             : b < kRecipCosWord  ? __builtin_bit_cast(uint32_t, kRecipDen16.v[b - kNanEntry - 1u])
-                                  : __builtin_bit_cast(uint32_t, kRecipCos16.v[b - kRecipCosWord]);
+    lut[b] = b < kRecipCosWord                   ? __builtin_bit_cast(uint32_t, kRecipDen16.v[b - kDenWord])
+             : b < kAngleWord                    ? __builtin_bit_cast(uint32_t, kRecipCos16.v[b - kRecipCosWord])
+             : b < kAngleWord + f16tab::kEntries ? kSinCos16.v[b - kAngleWord]
+                                                 : 0x7E007E00u;
   __syncthreads();
 
   const uint32_t lane = threadIdx.x & 63u, wave = threadIdx.x >> 6;
@@ -331,15 +340,14 @@ __global__ __launch_bounds__(kBlock16) void k_resident_f16x2(RolloutParams p) {
     // lane L computes both blocks' words of step tb + L
     const uint32_t g0 = uint32_t(__builtin_amdgcn_readfirstlane(int(e0))) >> 6;
     U2 b0{0u, 0u}, b1{0u, 0u};
-    uint32_t tb = 0u;
     auto step = [&](uint32_t j, auto any) {
       const uint32_t t = p.t0 + j;
       if (j == 0u || (t & 63u) == 0u) {
-        tb = t & ~63u;
+        const uint32_t tb = t & ~63u;
         b0 = threefry2x32(p.kact.a, p.kact.b, g0, tb + lane);
         b1 = threefry2x32(p.kact.a, p.kact.b, g0 + 1u, tb + lane);
       }
-      const int src = int(t - tb);
+      const int src = int(t & 63u);  // the words were computed at t & ~63
       const unsigned long long w0 =
           (static_cast<unsigned long long>(uint32_t(__builtin_amdgcn_readlane(int(b0.b), src)))
            << 32) | uint32_t(__builtin_amdgcn_readlane(int(b0.a), src));
