@@ -163,21 +163,25 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
     k0 = p.ep_index[i];
     len0 = p.ep_len[i];
   }
+  // The episode index is brought up to date at the refills only: while
+  // `have` holds the lane is in episode k, after a termination that used the
+  // prefetched start state it is in episode k + 1.
   uint32_t k = k0, len = len0;
   // Start state of the next episode, drawn ahead of time so that a
   // termination costs a select; `have` says whether it is drawn yet.
   S nxt = P::draw(p.krst, env, k + 1u);
   bool have = true;
-  unsigned long long wave_done = 0u;
   // One step (the j-th of this rollout).
   auto step = [&](uint32_t j) {
     const uint32_t t = p.t0 + j;
     const uint32_t a = policy(j, t, s);
     S o = P::step(s, a);
     const bool d = valid && P::done(o);
-    k += d ? 1u : 0u;
     len = d ? 0u : len + 1u;
-    if (d && !have) nxt = P::draw(p.krst, env, k);  // second termination before a refill
+    if (d && !have) {  // second termination before a refill
+      k += 1u;
+      nxt = P::draw(p.krst, env, k + 1u);
+    }
     if (d) o = nxt;
     have = have && !d;
     s = o;
@@ -185,7 +189,6 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
       if (off32) store_traj<true>(p, pobs, j, i, s, d);
       else store_traj<false>(p, pobs, j, i, s, d);
     }
-    wave_done += __popcll(__ballot(d));
   };
   // Steps in rounds of kRefill (unrolled: the refill test and the loop
   // control once per round), then the remaining steps.  After each round
@@ -196,11 +199,13 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
 #pragma unroll
     for (uint32_t r = 0; r < kRefill; ++r) step(j + r);
     if (!have) {
+      k += 1u;
       nxt = P::draw(p.krst, env, k + 1u);
       have = true;
     }
   }
   for (; j < p.T; ++j) step(j);
+  if (!have) k += 1u;
   // Over the rollout an environment's terminations are the growth of its
   // episode index and its finished returns are T + len(start) - len(end);
   // the summed reward of T steps (1 each, accumulated in binary32) is T up
@@ -225,7 +230,7 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
     }
     if (p.ret_sum) p.ret_sum[i] = (p.first ? 0u : p.ret_sum[i]) + returns;
   }
-  if (p.global) block_publish<kResidentBlock>(p.global, wave_done, valid ? returns : 0u, true);
+  if (p.global) block_publish<kResidentBlock>(p.global, n_done, valid ? returns : 0u, false);
 }
 
 }  // namespace cp
