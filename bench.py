@@ -325,6 +325,9 @@ def bench_launch_bound(cp, legs=("fused", "fused_direct", "concat", "unfused")):
 UNROLL_LADDER = (1, 2, 5, 10, 20, 50, 100, 250, 1000)
 
 
+TUNE_TOLERANCE = 0.05
+
+
 def bench_unroll(cp, K=1000):
     """The headline workload run by the register-resident kernel with k
     steps per launch (the paper's scan unroll factor, Sec. "Fusion via
@@ -339,9 +342,18 @@ def bench_unroll(cp, K=1000):
         wall, ev = timed(lambda: cp.cp_rollout(s, K, 0, None))
         out[str(k)] = {"us_per_step": wall * 1e3 / K, "env_steps_per_s": n * K / (wall * 1e-3)}
     best = min(out, key=lambda k: out[k]["us_per_step"])
+    # the library's own choice (cp_tune_steps_per_launch): the smallest
+    # candidate k within 5% of the fastest, measured on a copy of the state
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    cp.cp_init(s, 0)
+    tk, tus = cp.cp_tune_steps_per_launch(s, K, 0, tolerance=TUNE_TOLERANCE)
+    cands = [1, 2, 5, 10, 20, 50, 100, 200, 500, 1000, K]
+    tuned = {"tolerance": TUNE_TOLERANCE, "steps_per_launch": tk,
+             "us_per_step": {str(c): u for c, u in zip(cands, tus) if u == u}}
     return {"envs": n, "steps": K, "ladder": out, "best_steps_per_launch": int(best),
             "speedup_best_vs_1": out["1"]["us_per_step"] / out[best]["us_per_step"],
-            "speedup_10_vs_1": out["1"]["us_per_step"] / out["10"]["us_per_step"]}
+            "speedup_10_vs_1": out["1"]["us_per_step"] / out["10"]["us_per_step"],
+            "tuned": tuned}
 
 
 def bench_copy():

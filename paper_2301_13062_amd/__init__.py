@@ -82,6 +82,9 @@ def lib():
         L.cp_policy.restype = ctypes.c_int
         L.cp_policy_init.argtypes = [_p, ctypes.c_uint64]
         L.cp_policy_init.restype = ctypes.c_int
+        L.cp_tune_steps_per_launch.argtypes = [P(cp_states), ctypes.c_int64, ctypes.c_uint64,
+                                               ctypes.c_double, P(ctypes.c_int64), _p]
+        L.cp_tune_steps_per_launch.restype = ctypes.c_int
         L.cp_graph_replays.argtypes = []
         L.cp_graph_replays.restype = ctypes.c_uint64
         L.cp_workspace_bytes.argtypes = [ctypes.c_int64, ctypes.c_int32]
@@ -242,6 +245,24 @@ def cp_policy_init(seed: int):
     w = np.empty(CP_POLICY_WEIGHTS, dtype=np.uint16)
     _check(lib().cp_policy_init(w.ctypes.data, int(seed)))
     return w
+
+
+CP_TUNE_CANDIDATES = 11
+
+
+def cp_tune_steps_per_launch(states: CartPoleStates, n_steps: int, seed: int,
+                             tolerance: float = 0.05):
+    """The measured unroll factor (cartpole.h): returns (k, us_per_step),
+    k the smallest candidate steps_per_launch within `tolerance` of the
+    fastest, us_per_step the CP_TUNE_CANDIDATES measured times (NaN where
+    skipped).  The handle is not changed."""
+    h = states.handle()
+    k = ctypes.c_int64(0)
+    us = (ctypes.c_double * CP_TUNE_CANDIDATES)()
+    _check(lib().cp_tune_steps_per_launch(ctypes.byref(h), int(n_steps), int(seed),
+                                          float(tolerance), ctypes.byref(k),
+                                          ctypes.cast(us, ctypes.c_void_p)))
+    return int(k.value), list(us)
 
 
 def cp_graph_replays() -> int:

@@ -531,6 +531,96 @@ CP_API int cp_policy_init(uint16_t *host_w, uint64_t seed) {
   return ok();
 }
 
+CP_API int cp_tune_steps_per_launch(const cp_states *s, int64_t n_steps, uint64_t seed,
+                                    double tolerance, int64_t *best_k, double *us_per_step) {
+  if (int e = check_states(s)) return e;
+  if (!best_k) return fail(CP_ERR_NULL, "best_k is NULL");
+  if (s->variant != CP_RESIDENT)
+    return fail(CP_ERR_UNSUPPORTED, "steps per launch apply to CP_RESIDENT only");
+  if (n_steps < 1) return fail(CP_ERR_SIZE, "n_steps = %lld is below 1", (long long)n_steps);
+  if (!(tolerance >= 0.0) || !std::isfinite(tolerance))
+    return fail(CP_ERR_RANGE, "tolerance must be finite and non-negative");
+  const cp_traj none{};
+  if (int e = check_rollout(s, n_steps, none)) return e;
+
+  static const int64_t kCandidates[CP_TUNE_CANDIDATES - 1] = {1, 2, 5, 10, 20, 50, 100, 200, 500, 1000};
+  double us[CP_TUNE_CANDIDATES];
+  int64_t ks[CP_TUNE_CANDIDATES];
+  for (int c = 0; c < CP_TUNE_CANDIDATES; ++c) {
+    ks[c] = c + 1 < CP_TUNE_CANDIDATES ? kCandidates[c] : n_steps;
+    us[c] = std::nan("");
+  }
+  // a copy of the state to run on: four planes of the handle's precision,
+  // then ep_index and ep_len
+  hipStream_t st = static_cast<hipStream_t>(s->stream);
+  const size_t n = size_t(s->n), eb = elem_bytes(s->precision);
+  const size_t plane = n * eb, bytes = 4u * plane + 8u * n;
+  char *buf = nullptr;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  int rc = CP_OK;
+  auto cleanup = [&]() {
+    (void)hipStreamSynchronize(st);
+    if (e0) (void)hipEventDestroy(e0);
+    if (e1) (void)hipEventDestroy(e1);
+    if (buf) (void)hipFree(buf);
+  };
+  if ((rc = hip_status(hipMalloc(&buf, bytes), "cp_tune_steps_per_launch allocation"))) {
+    buf = nullptr;
+    return rc;
+  }
+  cp_states w = *s;
+  w.x = reinterpret_cast<float *>(buf);
+  w.x_dot = reinterpret_cast<float *>(buf + plane);
+  w.theta = reinterpret_cast<float *>(buf + 2u * plane);
+  w.theta_dot = reinterpret_cast<float *>(buf + 3u * plane);
+  w.ep_index = reinterpret_cast<uint32_t *>(buf + 4u * plane);
+  w.ep_len = reinterpret_cast<uint32_t *>(buf + 4u * plane + 4u * n);
+  const void *src[6] = {s->x, s->x_dot, s->theta, s->theta_dot, s->ep_index, s->ep_len};
+  void *dst[6] = {w.x, w.x_dot, w.theta, w.theta_dot, w.ep_index, w.ep_len};
+  const size_t len[6] = {plane, plane, plane, plane, 4u * n, 4u * n};
+  auto restore = [&]() -> int {
+    for (int a = 0; a < 6; ++a)
+      if (int r = hip_status(hipMemcpyAsync(dst[a], src[a], len[a], hipMemcpyDeviceToDevice, st),
+                             "cp_tune_steps_per_launch copy"))
+        return r;
+    return CP_OK;
+  };
+  if ((rc = hip_status(hipEventCreate(&e0), "event")) || (rc = hip_status(hipEventCreate(&e1), "event"))) {
+    cleanup();
+    return rc;
+  }
+  for (int c = 0; c < CP_TUNE_CANDIDATES && rc == CP_OK; ++c) {
+    if (ks[c] > n_steps || (c + 1 < CP_TUNE_CANDIDATES && ks[c] == n_steps)) continue;
+    w.steps_per_launch = ks[c];
+    float ms = 0.0f;
+    for (int rep = 0; rep < 2 && rc == CP_OK; ++rep) {  // an untimed rollout, then the timed one
+      if ((rc = restore())) break;
+      w.t = s->t;
+      if ((rc = hip_status(hipEventRecord(e0, st), "event"))) break;
+      if ((rc = run_rollout(&w, n_steps, seed, none, nullptr, false))) break;
+      if ((rc = hip_status(hipEventRecord(e1, st), "event"))) break;
+      if ((rc = hip_status(hipEventSynchronize(e1), "event"))) break;
+      if ((rc = hip_status(hipEventElapsedTime(&ms, e0, e1), "event"))) break;
+    }
+    us[c] = 1e3 * double(ms) / double(n_steps);
+  }
+  cleanup();
+  if (rc != CP_OK) return rc;
+  double fastest = HUGE_VAL;
+  for (int c = 0; c < CP_TUNE_CANDIDATES; ++c)
+    if (us[c] == us[c] && us[c] < fastest) fastest = us[c];
+  int64_t pick = n_steps;
+  for (int c = 0; c < CP_TUNE_CANDIDATES; ++c)
+    if (us[c] == us[c] && us[c] <= (1.0 + tolerance) * fastest) {
+      pick = ks[c];
+      break;
+    }
+  *best_k = pick;
+  if (us_per_step)
+    for (int c = 0; c < CP_TUNE_CANDIDATES; ++c) us_per_step[c] = us[c];
+  return ok();
+}
+
 CP_API uint64_t cp_graph_replays(void) { return cp::graph_replays(); }
 
 CP_API size_t cp_workspace_bytes(int64_t n, int32_t variant) {

@@ -432,3 +432,31 @@ def test_noalloc_validates_before_any_hip_call():
     h = handle(variant=cp.CP_FUSED, policy_w=A + 0x900000)
     assert L.cp_rollout_noalloc(ctypes.byref(h), 2, 0, None) == cp.CP_ERR_UNSUPPORTED
     assert h.t == 7
+
+
+def call_tune(h, n_steps=10, tol=0.05, best=True, us=None):
+    k = ctypes.c_int64(-1)
+    return cp.lib().cp_tune_steps_per_launch(
+        ctypes.byref(h) if h is not None else None, n_steps, 0, tol,
+        ctypes.byref(k) if best else None, us), k.value
+
+
+@pytest.mark.parametrize("kw,args,code", [
+    ({}, {}, cp.CP_ERR_UNSUPPORTED),                                   # not CP_RESIDENT
+    ({"variant": cp.CP_RESIDENT}, {"n_steps": 0}, cp.CP_ERR_SIZE),
+    ({"variant": cp.CP_RESIDENT}, {"n_steps": -3}, cp.CP_ERR_SIZE),
+    ({"variant": cp.CP_RESIDENT}, {"tol": -0.1}, cp.CP_ERR_RANGE),
+    ({"variant": cp.CP_RESIDENT}, {"tol": float("nan")}, cp.CP_ERR_RANGE),
+    ({"variant": cp.CP_RESIDENT}, {"tol": float("inf")}, cp.CP_ERR_RANGE),
+    ({"variant": cp.CP_RESIDENT}, {"best": False}, cp.CP_ERR_NULL),
+    ({"variant": cp.CP_RESIDENT, "x": None}, {}, cp.CP_ERR_NULL),
+    ({"variant": cp.CP_RESIDENT, "t": 2 ** 31 - 5}, {}, cp.CP_ERR_RANGE),
+])
+def test_tune_rejects_bad_calls(kw, args, code):
+    # every rejection comes before any HIP call (there is no GPU here)
+    h = handle(**kw)
+    rc, k = call_tune(h, **args)
+    assert rc == code and k == -1
+    assert cp.lib().cp_last_error().decode() != ""
+    assert h.t == kw.get("t", 7)
+    assert call_tune(None)[0] == cp.CP_ERR_NULL

@@ -259,6 +259,36 @@ def test_unroll_ladder_matches_oracle(gpu, k):
     assert tot[0] == u32(tr.done_count).sum() and tot[1] == u32(tr.ret_sum).sum()
 
 
+def test_tuned_steps_per_launch(gpu):
+    # The measured unroll factor (cp_tune_steps_per_launch) on the same
+    # workload: the handle is left as it was, the chosen k is the smallest
+    # candidate within the tolerance of the fastest, and a rollout at that k
+    # matches the oracle's as every k does.
+    n, T, tol = 65536, 1000, 0.1
+    s = cp.CartPoleStates(n, variant=cp.CP_RESIDENT)
+    cp.cp_init(s, 0)
+    before = (s.state().clone(), s.ep_index.clone(), s.ep_len.clone(), s.t)
+    k, us = cp.cp_tune_steps_per_launch(s, T, 0, tolerance=tol)
+    torch.cuda.synchronize()
+    assert torch.equal(s.state(), before[0]) and torch.equal(s.ep_index, before[1])
+    assert torch.equal(s.ep_len, before[2]) and s.t == before[3]
+    cands = [1, 2, 5, 10, 20, 50, 100, 200, 500, 1000, T]
+    measured = {c: u for c, u in zip(cands, us) if u == u}
+    assert sorted(measured) == [1, 2, 5, 10, 20, 50, 100, 200, 500, T]  # 1000 == T: measured once
+    assert all(u > 0 for u in measured.values())
+    fastest = min(measured.values())
+    assert k in measured and measured[k] <= (1 + tol) * fastest
+    assert all(measured[c] > (1 + tol) * fastest for c in measured if c < k)
+    s.steps_per_launch = k
+    tr = cp.Trajectory(n, T, obs=False, reward=False)
+    cp.cp_rollout(s, T, 0, tr)
+    torch.cuda.synchronize()
+    o, out = _oracle_65536x1000()
+    g, gk, gl = gpu_state(s)
+    match = assert_rollout_match(tr.done.cpu().numpy(), out["done"], g, o.state())
+    assert np.array_equal(gk[match], o.ep_index[match]) and np.array_equal(gl[match], o.ep_len[match])
+
+
 def _sample_ids(n, k, seed):
     rng = np.random.default_rng(seed)
     ids = np.unique(np.concatenate([rng.choice(n, k, replace=False), [0, n - 1]]))
