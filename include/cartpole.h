@@ -260,22 +260,26 @@ int cp_policy_init(uint16_t *host_w, uint64_t seed);
  * MLP policy; no trajectory) at each candidate steps_per_launch
  *     k = 1, 2, 5, 10, 20, 50, 100, 200, 500, 1000, n_steps
  * (those above n_steps skipped), each after one untimed rollout, on a copy
- * of the handle's state that the call allocates and frees (the handle's own
- * arrays and step counter are not changed), and returns in *best_k the
+ * of the handle's state in `scratch` (device memory of at least
+ * n * (4 * element bytes of the handle's precision + 8) bytes, 8-byte
+ * aligned, sharing no byte with the state arrays; the handle's own arrays
+ * and step counter are not changed), and returns in *best_k the
  * smallest k whose time per step is at most (1 + tolerance) times the
  * fastest candidate's: the most frequent write-back of the state to HBM
  * (the shortest launches) that costs at most that fraction.  Results of a
  * rollout do not depend on k.  us_per_step, if not NULL, receives the
  * CP_TUNE_CANDIDATES measured times in microseconds per step, in the order
  * above (NaN for a skipped candidate).  Synchronises the handle's stream.
- * Returns CP_OK; CP_ERR_NULL (s or best_k NULL, or a state array NULL),
- * CP_ERR_UNSUPPORTED (not CP_RESIDENT), CP_ERR_SIZE (n_steps < 1),
- * CP_ERR_RANGE (tolerance negative or not finite, or the step counter would
- * pass 2^31), the other errors of cp_rollout (all checked before any HIP
- * call), or CP_ERR_HIP.                                                      */
+ * Returns CP_OK; CP_ERR_NULL (s, scratch or best_k NULL, or a state array
+ * NULL), CP_ERR_UNSUPPORTED (not CP_RESIDENT), CP_ERR_SIZE (n_steps < 1, or
+ * scratch_bytes too small), CP_ERR_ALIGN (scratch), CP_ERR_OVERLAP (scratch
+ * and the state arrays), CP_ERR_RANGE (tolerance negative or not finite, or
+ * the step counter would pass 2^31), the other errors of cp_rollout (all
+ * checked before any HIP call), or CP_ERR_HIP.                              */
 #define CP_TUNE_CANDIDATES 11
 int cp_tune_steps_per_launch(const cp_states *s, int64_t n_steps, uint64_t seed,
-                             double tolerance, int64_t *best_k, double *us_per_step);
+                             double tolerance, void *scratch, size_t scratch_bytes,
+                             int64_t *best_k, double *us_per_step);
 
 /* Number of cp_rollout calls in this process whose steps were replayed from
  * a cached HIP graph (CP_FUSED with a workspace, above), for callers and

@@ -83,7 +83,8 @@ def lib():
         L.cp_policy_init.argtypes = [_p, ctypes.c_uint64]
         L.cp_policy_init.restype = ctypes.c_int
         L.cp_tune_steps_per_launch.argtypes = [P(cp_states), ctypes.c_int64, ctypes.c_uint64,
-                                               ctypes.c_double, P(ctypes.c_int64), _p]
+                                               ctypes.c_double, _p, ctypes.c_size_t,
+                                               P(ctypes.c_int64), _p]
         L.cp_tune_steps_per_launch.restype = ctypes.c_int
         L.cp_graph_replays.argtypes = []
         L.cp_graph_replays.restype = ctypes.c_uint64
@@ -255,13 +256,19 @@ def cp_tune_steps_per_launch(states: CartPoleStates, n_steps: int, seed: int,
     """The measured unroll factor (cartpole.h): returns (k, us_per_step),
     k the smallest candidate steps_per_launch within `tolerance` of the
     fastest, us_per_step the CP_TUNE_CANDIDATES measured times (NaN where
-    skipped).  The handle is not changed."""
+    skipped).  The handle is not changed; the state copy the trials run on
+    is a torch buffer."""
     h = states.handle()
+    n = int(states.n)
+    scratch = torch.empty(n * (4 * states.x.element_size() + 8), dtype=torch.uint8,
+                          device=states.x.device)
     k = ctypes.c_int64(0)
     us = (ctypes.c_double * CP_TUNE_CANDIDATES)()
     _check(lib().cp_tune_steps_per_launch(ctypes.byref(h), int(n_steps), int(seed),
-                                          float(tolerance), ctypes.byref(k),
-                                          ctypes.cast(us, ctypes.c_void_p)))
+                                          float(tolerance), _ptr(scratch), scratch.numel(),
+                                          ctypes.byref(k), ctypes.cast(us, ctypes.c_void_p)))
+    torch.cuda.synchronize(states.x.device)
+    del scratch
     return int(k.value), list(us)
 
 

@@ -532,9 +532,10 @@ CP_API int cp_policy_init(uint16_t *host_w, uint64_t seed) {
 }
 
 CP_API int cp_tune_steps_per_launch(const cp_states *s, int64_t n_steps, uint64_t seed,
-                                    double tolerance, int64_t *best_k, double *us_per_step) {
+                                    double tolerance, void *scratch, size_t scratch_bytes,
+                                    int64_t *best_k, double *us_per_step) {
   if (int e = check_states(s)) return e;
-  if (!best_k) return fail(CP_ERR_NULL, "best_k is NULL");
+  if (!best_k || !scratch) return fail(CP_ERR_NULL, "best_k or scratch is NULL");
   if (s->variant != CP_RESIDENT)
     return fail(CP_ERR_UNSUPPORTED, "steps per launch apply to CP_RESIDENT only");
   if (n_steps < 1) return fail(CP_ERR_SIZE, "n_steps = %lld is below 1", (long long)n_steps);
@@ -542,6 +543,15 @@ CP_API int cp_tune_steps_per_launch(const cp_states *s, int64_t n_steps, uint64_
     return fail(CP_ERR_RANGE, "tolerance must be finite and non-negative");
   const cp_traj none{};
   if (int e = check_rollout(s, n_steps, none)) return e;
+  const size_t n = size_t(s->n), eb = elem_bytes(s->precision);
+  const size_t plane = n * eb, bytes = 4u * plane + 8u * n;
+  if (scratch_bytes < bytes)
+    return fail(CP_ERR_SIZE, "scratch has %zu bytes, the state copy needs %zu", scratch_bytes, bytes);
+  if (reinterpret_cast<uintptr_t>(scratch) & 7u) return fail(CP_ERR_ALIGN, "scratch must be 8-byte aligned");
+  {
+    const Range r = range_of(scratch, bytes, "scratch");
+    if (int e = check_overlap(s, &r, 1)) return e;
+  }
 
   static const int64_t kCandidates[CP_TUNE_CANDIDATES - 1] = {1, 2, 5, 10, 20, 50, 100, 200, 500, 1000};
   double us[CP_TUNE_CANDIDATES];
@@ -550,24 +560,17 @@ CP_API int cp_tune_steps_per_launch(const cp_states *s, int64_t n_steps, uint64_
     ks[c] = c + 1 < CP_TUNE_CANDIDATES ? kCandidates[c] : n_steps;
     us[c] = std::nan("");
   }
-  // a copy of the state to run on: four planes of the handle's precision,
-  // then ep_index and ep_len
+  // the copy of the state to run on, in the scratch: four planes of the
+  // handle's precision, then ep_index and ep_len
   hipStream_t st = static_cast<hipStream_t>(s->stream);
-  const size_t n = size_t(s->n), eb = elem_bytes(s->precision);
-  const size_t plane = n * eb, bytes = 4u * plane + 8u * n;
-  char *buf = nullptr;
+  char *const buf = static_cast<char *>(scratch);
   hipEvent_t e0 = nullptr, e1 = nullptr;
   int rc = CP_OK;
   auto cleanup = [&]() {
     (void)hipStreamSynchronize(st);
     if (e0) (void)hipEventDestroy(e0);
     if (e1) (void)hipEventDestroy(e1);
-    if (buf) (void)hipFree(buf);
   };
-  if ((rc = hip_status(hipMalloc(&buf, bytes), "cp_tune_steps_per_launch allocation"))) {
-    buf = nullptr;
-    return rc;
-  }
   cp_states w = *s;
   w.x = reinterpret_cast<float *>(buf);
   w.x_dot = reinterpret_cast<float *>(buf + plane);

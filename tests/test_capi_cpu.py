@@ -434,10 +434,13 @@ def test_noalloc_validates_before_any_hip_call():
     assert h.t == 7
 
 
-def call_tune(h, n_steps=10, tol=0.05, best=True, us=None):
+SCRATCH = A + 0x100000  # 1000 envs x (4 x 4 + 8) bytes fit below the next 1 MiB
+
+
+def call_tune(h, n_steps=10, tol=0.05, best=True, us=None, scratch=SCRATCH, scratch_bytes=24000):
     k = ctypes.c_int64(-1)
     return cp.lib().cp_tune_steps_per_launch(
-        ctypes.byref(h) if h is not None else None, n_steps, 0, tol,
+        ctypes.byref(h) if h is not None else None, n_steps, 0, tol, scratch, scratch_bytes,
         ctypes.byref(k) if best else None, us), k.value
 
 
@@ -451,6 +454,10 @@ def call_tune(h, n_steps=10, tol=0.05, best=True, us=None):
     ({"variant": cp.CP_RESIDENT}, {"best": False}, cp.CP_ERR_NULL),
     ({"variant": cp.CP_RESIDENT, "x": None}, {}, cp.CP_ERR_NULL),
     ({"variant": cp.CP_RESIDENT, "t": 2 ** 31 - 5}, {}, cp.CP_ERR_RANGE),
+    ({"variant": cp.CP_RESIDENT}, {"scratch": None}, cp.CP_ERR_NULL),
+    ({"variant": cp.CP_RESIDENT}, {"scratch_bytes": 23999}, cp.CP_ERR_SIZE),
+    ({"variant": cp.CP_RESIDENT}, {"scratch": SCRATCH + 4}, cp.CP_ERR_ALIGN),
+    ({"variant": cp.CP_RESIDENT}, {"scratch": A + 0x3000}, cp.CP_ERR_OVERLAP),  # over theta_dot
 ])
 def test_tune_rejects_bad_calls(kw, args, code):
     # every rejection comes before any HIP call (there is no GPU here)
