@@ -283,3 +283,37 @@ def test_f16_rollout_longer_than_one_launch(gpu):
         assert np.array_equal(getattr(tr, f).cpu().numpy().view(np.uint32), out[f]), f
     tot = tr.totals.cpu().numpy()
     assert tot[0] == out["done_count"].sum() and tot[1] == out["ret_sum"].sum()
+
+
+@pytest.mark.parametrize("prec,env_base", [("f16", 0), ("f16", 5), ("f64", 0)])
+def test_every_environment_resets_at_once(gpu, prec, env_base):
+    # every environment starts beyond the angle limit, so all terminate at the
+    # first step and all ask for their next start state at the same refill
+    # (in the two-per-lane binary16 kernel: 128 requests of a wave, served in
+    # two passes of the exchange); then 40 steps on, bit for bit (binary16)
+    # or within the binary64 bound as the oracle
+    n, T = 4 * 128 + 64, 41
+    st4 = np.zeros((4, n))
+    st4[2] = np.where(np.arange(n) % 2 == 0, 0.5, -0.5)
+    st4 = st4.astype(PRECS[prec][2])
+    s = handle(n, prec, env_base)
+    for dst, src in zip((s.x, s.x_dot, s.theta, s.theta_dot), st4):
+        dst.copy_(torch.from_numpy(np.ascontiguousarray(src)))
+    s.ep_index.zero_()
+    s.ep_len.zero_()
+    s.seed, s.t = 21, 0
+    tr = traj(n, T, prec)
+    cp.cp_rollout(s, T, 22, tr)
+    torch.cuda.synchronize()
+    o = oracle_state(n, prec, np.arange(env_base, env_base + n))
+    o.x, o.x_dot, o.theta, o.theta_dot = (np.ascontiguousarray(v) for v in st4)
+    o.ep_index, o.ep_len = np.zeros(n, np.uint32), np.zeros(n, np.uint32)
+    o.seed, o.t = 21, 0
+    out = O.rollout_prec(o, T, act_seed=22, traj=True)
+    done = tr.done.cpu().numpy()
+    assert done[0].all() and np.array_equal(done[0], out["done"][0])
+    g, gk, gl = gpu_state(s)
+    match = check_rollout(prec, done, out["done"], g, o.state())
+    assert np.array_equal(gk[match], o.ep_index[match]) and np.array_equal(gl[match], o.ep_len[match])
+    for f in ("done_count", "ret_sum"):
+        assert np.array_equal(getattr(tr, f).cpu().numpy().view(np.uint32)[match], out[f][match]), f
