@@ -31,10 +31,11 @@
  *    before any HIP call: on CP_ERR_NULL/SIZE/ALIGN/RANGE/UNSUPPORTED/OVERLAP
  *    nothing is launched and *s is unchanged.  CP_ERR_HIP reports a failed
  *    launch; the handle's arrays then hold unspecified values.
- *  - Outputs must not overlap the state arrays or each other: cp_step and
- *    cp_rollout compare the byte ranges of every output they are given with
- *    those of the state arrays and of the other outputs, and return
- *    CP_ERR_OVERLAP when two share a byte.
+ *  - Outputs must not overlap the state arrays, the policy weights or each
+ *    other: cp_step, cp_rollout and cp_tune_steps_per_launch compare the
+ *    byte ranges of every output they are given with those of the state
+ *    arrays, of the handle's policy weights (if set) and of the other
+ *    outputs, and return CP_ERR_OVERLAP when two share a byte.
  *  - A cp_states handle is not thread-safe; distinct handles are independent.
  */
 #ifndef CARTPOLE_H
@@ -62,7 +63,7 @@ extern "C" {
 #define CP_ERR_RANGE (-4)       /* step counter or environment index would overflow   */
 #define CP_ERR_HIP (-5)         /* a HIP launch failed; see cp_last_error()           */
 #define CP_ERR_UNSUPPORTED (-6) /* combination not provided (e.g. policy + UNFUSED)    */
-#define CP_ERR_OVERLAP (-7)     /* an output shares memory with the state or another output */
+#define CP_ERR_OVERLAP (-7)     /* an output shares memory with the state, the weights or another output */
 
 /* Precision of the state, the step and the obs trajectory
  * (cp_states.precision).  The paper's own implementation is binary32; the

@@ -123,7 +123,8 @@ Range range_of(const void *p, unsigned __int128 bytes, const char *name) {
   return Range{lo, lo + bytes, name};
 }
 
-// The state arrays of a handle (6 ranges).
+// The state arrays of a handle and its policy weights if set (6 or 7
+// ranges): what no output may share a byte with.
 int state_ranges(const cp_states *s, Range *out) {
   const unsigned __int128 n = uint64_t(s->n), eb = elem_bytes(s->precision);
   out[0] = range_of(s->x, n * eb, "x");
@@ -132,13 +133,15 @@ int state_ranges(const cp_states *s, Range *out) {
   out[3] = range_of(s->theta_dot, n * eb, "theta_dot");
   out[4] = range_of(s->ep_index, n * 4u, "ep_index");
   out[5] = range_of(s->ep_len, n * 4u, "ep_len");
-  return 6;
+  if (!s->policy_w) return 6;
+  out[6] = range_of(s->policy_w, 2u * CP_POLICY_WEIGHTS, "policy_w");
+  return 7;
 }
 
 // CP_ERR_OVERLAP unless every output range is disjoint from every state
-// range and from every other output range.
+// range (and the weights) and from every other output range.
 int check_overlap(const cp_states *s, const Range *outs, int n_outs) {
-  Range st[6];
+  Range st[7];
   const int n_st = state_ranges(s, st);
   auto meet = [](const Range &a, const Range &b) { return a.lo < b.hi && b.lo < a.hi; };
   for (int i = 0; i < n_outs; ++i) {

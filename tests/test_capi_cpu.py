@@ -350,6 +350,10 @@ def test_rollout_outputs_overlapping_are_refused():
     assert go(reward=FAR, done_count=FAR + T * n * 4 - 4) == cp.CP_ERR_OVERLAP
     assert go(ret_sum=FAR, **{"global": FAR + 3992}) == cp.CP_ERR_OVERLAP
     assert go(total_reward=FAR, ret_sum=FAR) == cp.CP_ERR_OVERLAP
+    # outputs over the policy weights (4480 bf16 values at A + 0x900000)
+    assert go(done_count=A + 0x900000 + 8960 - 4) == cp.CP_ERR_OVERLAP
+    assert "policy_w" in cp.lib().cp_last_error().decode()
+    assert go(reward=A + 0x900000 - T * n * 4 + 4) == cp.CP_ERR_OVERLAP
     # the whole trajectory laid out back to back: no overlap, next check fails
     assert go(obs=FAR, reward=FAR + obs_bytes, done=FAR + obs_bytes + T * n * 4,
               done_count=FAR + 0x100000, total_reward=FAR + 0x101000, ret_sum=FAR + 0x102000,
