@@ -205,9 +205,18 @@ __device__ __forceinline__ float div_rn(float a, float b) {
 //   xacc  = temp - ((pml * thacc) * cos) / M
 __device__ __forceinline__ float force_of(uint32_t a) { return a ? kForceMag : -kForceMag; }
 
+// kLimited: the angle is one a step produces -- within the 12-degree limit,
+// or NaN -- so the polynomials alone give the same values (a NaN angle gives
+// NaN either way); a caller's state may hold any angle (kLimited false).
+template <bool kLimited = false>
 __device__ __forceinline__ State dynamics(State s, float force) {
   float sn, c;
-  sincos_th(s.th, sn, c);
+  if (kLimited) {
+    sn = sin_small(s.th);
+    c = cos_small(s.th);
+  } else {
+    sincos_th(s.th, sn, c);
+  }
   const float thd2 = s.thd * s.thd;
   const float c2 = c * c;
   const float temp = div_mass(force + kPoleMassLength * thd2 * sn);

@@ -36,8 +36,10 @@ struct PrecF32 {
   __device__ static __forceinline__ S draw(U2 key, uint32_t env, uint32_t k) {
     return reset_draw(key, env, k);
   }
+  // kLimited: the state's angle is within the limit or NaN (see dynamics)
+  template <bool kLimited = false>
   __device__ static __forceinline__ S step(const S &s, uint32_t a) {
-    return dynamics(s, force_of(a));
+    return dynamics<kLimited>(s, force_of(a));
   }
   __device__ static __forceinline__ bool done(const S &s) { return terminated(s); }
 };
@@ -110,11 +112,18 @@ __device__ __forceinline__ double div_mass64(double x) {
   return __builtin_fma(r, kInvTotalMass64, q);
 }
 
+// kLimited as for dynamics: an angle within the limit or NaN.
+template <bool kLimited = false>
 __device__ __forceinline__ State64 dynamics64(const State64 &s, double force) {
   const double g = 9.8, mp = 0.1, l = 0.5, tau = 0.02;
   const double pml = mp * l, four3 = 4.0 / 3.0;
   double sn, c;
-  sincos64(s.th, sn, c);
+  if (kLimited) {
+    sn = sin_small64(s.th);
+    c = cos_small64(s.th);
+  } else {
+    sincos64(s.th, sn, c);
+  }
   const double thd2 = s.thd * s.thd;
   const double c2 = c * c;
   const double temp = div_mass64(force + pml * thd2 * sn);
@@ -132,8 +141,9 @@ struct PrecF64 {
     return S{reset_value64(w.a & 0xFFFFu), reset_value64(w.a >> 16),
              reset_value64(w.b & 0xFFFFu), reset_value64(w.b >> 16)};
   }
+  template <bool kLimited = false>
   __device__ static __forceinline__ S step(const S &s, uint32_t a) {
-    return dynamics64(s, a ? 10.0 : -10.0);
+    return dynamics64<kLimited>(s, a ? 10.0 : -10.0);
   }
   __device__ static __forceinline__ bool done(const S &s) {
     return s.x < -2.4 || s.x > 2.4 || s.th < -kThetaLimit64 || s.th > kThetaLimit64;
@@ -236,6 +246,7 @@ struct PrecF16 {
     const State f = reset_draw(key, env, k);
     return S{to_half(f.x), to_half(f.xd), to_half(f.th), to_half(f.thd)};
   }
+  template <bool kLimited = false>  // the binary16 step makes no use of it
   __device__ static __forceinline__ S step(const S &s, uint32_t a) {
     return dynamics16(s, a ? half_t(10.0) : half_t(-10.0));
   }

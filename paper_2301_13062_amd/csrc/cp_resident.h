@@ -10,6 +10,8 @@
 // combines its waves in LDS and publishes the totals with one atomic pair.
 #pragma once
 
+#include <type_traits>
+
 #include "cp_launch.h"
 #include "cp_precision.h"
 
@@ -171,11 +173,13 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
   // termination costs a select; `have` says whether it is drawn yet.
   S nxt = P::draw(p.krst, env, k + 1u);
   bool have = true;
-  // One step (the j-th of this rollout).
-  auto step = [&](uint32_t j) {
+  // One step (the j-th of this rollout); `limited`: the state is one a step
+  // produced (every step after a launch's first), its angle within the
+  // limit or NaN.
+  auto step = [&](uint32_t j, auto limited) {
     const uint32_t t = p.t0 + j;
     const uint32_t a = policy(j, t, s);
-    S o = P::step(s, a);
+    S o = P::template step<decltype(limited)::value>(s, a);
     const bool d = valid && P::done(o);
     len = d ? 0u : len + 1u;
     if (d && !have) {  // second termination before a refill
@@ -244,17 +248,20 @@ __device__ __forceinline__ void resident_rollout(const RolloutParams &p, Policy 
       have = true;
     }
   };
-  // Steps in rounds of kRefill (unrolled: the refill test and the loop
-  // control once per round), each followed by the refill, then the
-  // remaining steps.
-  uint32_t j = 0;
+  // The launch's first step (any state), then rounds of kRefill steps
+  // (unrolled: the refill test and the loop control once per round), each
+  // followed by the refill, then the remaining steps.
+  using any_angle = std::integral_constant<bool, false>;
+  using limited_angle = std::integral_constant<bool, true>;
+  if (p.T > 0u) step(0u, any_angle{});
+  uint32_t j = 1;
   for (; j + kRefill <= p.T; j += kRefill) {
 #pragma unroll
-    for (uint32_t r = 0; r < kRefill; ++r) step(j + r);
+    for (uint32_t r = 0; r < kRefill; ++r) step(j + r, limited_angle{});
     if constexpr (kTraj) refill_block();
     else refill_wave();
   }
-  for (; j < p.T; ++j) step(j);
+  for (; j < p.T; ++j) step(j, limited_angle{});
   if (!have) k += 1u;
   // Over the rollout an environment's terminations are the growth of its
   // episode index and its finished returns are T + len(start) - len(end);
