@@ -41,7 +41,7 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const void *base, u
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, int(bytes), 0x00020000);
 }
 // Cache bits of the streaming rollout's trajectory stores: nt (streaming)
-// and sc1 (system scope), the combination measured fastest for these write
+// and sc1 (device scope), the combination measured fastest for these write
 // streams (nt alone 2% slower, plain or sc1-only stores 25-40% slower).
 constexpr int kStreamStoreAux = 2 | 16;
 __device__ __forceinline__ void stream_store(float v, __amdgpu_buffer_rsrc_t r, int off) {
