@@ -124,6 +124,57 @@ def test_fused_rollout_with_trajectory_at_the_offset_limit(gpu, n):
 
 
 @pytest.mark.parametrize("n", SIZES, ids=IDS)
+def test_streaming_terminations_at_the_offset_limit(gpu, n):
+    # The streaming rollout's first and middle steps update the episode
+    # counters of terminating lanes only.  Sampled environments (up to the
+    # top of the range) start where they terminate at step 0 or at step 1
+    # whatever the actions, with arbitrary starting counters, so that those
+    # updates and the reset draws they key run at the largest offsets.
+    seed, act_seed, T = 28, 29, 3
+    ids = sample(n, 5)
+    idx = torch.from_numpy(ids).cuda()
+    s = cp.CartPoleStates(n, variant=cp.CP_FUSED)
+    cp.cp_init(s, seed)
+    o = O.OracleState(len(ids), ids.astype(np.uint32))
+    O.init(o, seed)
+    rng = np.random.default_rng(6)
+    kind = rng.integers(0, 3, len(ids))
+    # x + tau x_dot passes 2.4 at once (kind 1), or only at the second step,
+    # where x_dot has moved by at most tau * 10 N / 1.1 kg plus the pole term
+    o.x[kind == 1], o.x_dot[kind == 1] = np.float32(2.399), np.float32(0.1)
+    o.x[kind == 2], o.x_dot[kind == 2] = np.float32(2.39), np.float32(0.35)
+    o.ep_index[:] = rng.integers(0, 1 << 31, len(ids), dtype=np.uint32)
+    o.ep_len[:] = rng.integers(0, 500, len(ids), dtype=np.uint32)
+    for a, v in ((s.x, o.x), (s.x_dot, o.x_dot), (s.theta, o.theta), (s.theta_dot, o.theta_dot)):
+        a.index_copy_(0, idx, torch.from_numpy(v).cuda())
+    for a, v in ((s.ep_index, o.ep_index), (s.ep_len, o.ep_len)):
+        a.index_copy_(0, idx, torch.from_numpy(v.view(np.int32)).cuda())
+    tr = cp.Trajectory(n, T, totals=False)
+    cp.cp_rollout(s, T, act_seed, tr)
+    torch.cuda.synchronize()
+    g_obs = cols(tr.obs, idx)
+    g_done = cols(tr.done, idx)
+    out = O.rollout(o, T, act_seed=act_seed, traj=True)
+    # the constructed terminations happen where they were placed
+    assert (out["done"][0][kind == 1] == 1).all() and (out["done"][1][kind == 2] == 1).all()
+    match = (g_done == out["done"]).all(axis=0)
+    assert match.mean() >= ROLL_MATCH and match[kind != 0].all()
+    err = np.abs(g_obs[:, :, match].astype(np.float64) - out["obs"][:, :, match])
+    assert err.max() <= ROLL_ABS
+    # a termination's reset state is the draw keyed by the new episode index
+    for step, kd in ((0, 1), (1, 2)):
+        sel = kind == kd
+        assert np.array_equal(g_obs[step][:, sel], out["obs"][step][:, sel])
+    k, ln = counters_at(s, idx)
+    assert np.array_equal(k[match], o.ep_index[match]) and np.array_equal(ln[match], o.ep_len[match])
+    for name in ("done_count", "ret_sum"):
+        g = cols(getattr(tr, name), idx).view(np.uint32)
+        assert np.array_equal(g[match], out[name][match]), name
+    del s, tr
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("n", SIZES, ids=IDS)
 def test_resident_rollout_with_trajectory_at_the_offset_limit(gpu, n):
     # the whole-rollout kernel's trajectory stores: each step's planes from
     # scalar bases with the lane's fixed 32-bit offset below the limit
