@@ -443,6 +443,48 @@ def test_resume_and_sharding_bit_exact(gpu, variant):
     assert torch.equal(ltr.totals + htr.totals, ftr.totals)
 
 
+def test_streaming_resume_sharding_and_fused_step_agree(gpu):
+    # From 2^21 environments a fused rollout with an obs trajectory streams
+    # (each step reads its state from the previous obs plane, the counters
+    # are touched at terminations only and rebuilt by the last step).  Split
+    # in time, split into two streaming shards by env_base, and run without
+    # an obs trajectory (the fused step on the state arrays), it gives the
+    # same bits.
+    n, T1, T2 = (1 << 22) + 1234, 30, 25
+    full, ftr = run(cp.CP_FUSED, n, T1 + T2, seed=9)
+    s = cp.CartPoleStates(n, variant=cp.CP_FUSED)
+    cp.cp_init(s, 9)
+    a, b = cp.Trajectory(n, T1), cp.Trajectory(n, T2)
+    cp.cp_rollout(s, T1, 9, a)
+    cp.cp_rollout(s, T2, 9, b)
+    torch.cuda.synchronize()
+    assert all(np.array_equal(x, y) for x, y in zip(gpu_state(s), gpu_state(full)))
+    for f in ("obs", "reward", "done"):
+        assert torch.equal(torch.cat([getattr(a, f), getattr(b, f)]), getattr(ftr, f)), f
+    # per-rollout statistics add up: terminations, finished returns (an
+    # episode crossing the split counts in the second rollout), T each
+    for f in ("done_count", "ret_sum", "total_reward", "totals"):
+        assert torch.equal(getattr(a, f) + getattr(b, f), getattr(ftr, f)), f
+    del s, a, b
+    cut = (1 << 21) + 77
+    lo, ltr = run(cp.CP_FUSED, cut, T1 + T2, seed=9)
+    hi, htr = run(cp.CP_FUSED, n - cut, T1 + T2, seed=9, env_base=cut)
+    for x, y, z in zip(gpu_state(lo), gpu_state(hi), gpu_state(full)):
+        assert np.array_equal(np.concatenate([x, y], axis=-1), z)
+    for f in ("obs", "reward", "done"):
+        assert torch.equal(torch.cat([getattr(ltr, f), getattr(htr, f)], -1), getattr(ftr, f)), f
+    for f in ("done_count", "ret_sum", "total_reward"):
+        assert torch.equal(torch.cat([getattr(ltr, f), getattr(htr, f)]), getattr(ftr, f)), f
+    assert torch.equal(ltr.totals + htr.totals, ftr.totals)
+    del lo, ltr, hi, htr
+    nf, ntr = run(cp.CP_FUSED, n, T1 + T2, seed=9, obs=False)
+    assert all(np.array_equal(x, y) for x, y in zip(gpu_state(nf), gpu_state(full)))
+    for f in ("reward", "done", "done_count", "ret_sum", "total_reward", "totals"):
+        assert torch.equal(getattr(ntr, f), getattr(ftr, f)), f
+    del nf, ntr, full, ftr
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
 def test_steps_equal_rollout(gpu, variant):
     n, T = 777, 40
