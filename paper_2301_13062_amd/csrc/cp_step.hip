@@ -35,17 +35,21 @@ constexpr uint32_t kEagerMaxEnvs = kObsStateMinEnvs;
 constexpr uint32_t kOff32MaxEnvs = 1u << 30;
 static_assert(kEagerMaxEnvs <= kOff32MaxEnvs, "the latency-oriented step uses 32-bit offsets");
 
-// Buffer resource of one plane (bytes < 2^32): raw 32-bit byte offsets,
-// accesses past `bytes` dropped by the hardware.
+// Buffer resource of one plane (bytes < 2^32): raw 32-bit byte offsets;
+// the hardware drops a store past `bytes` and returns 0 for such a load.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rsrc(const void *base, uint32_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, int(bytes), 0x00020000);
 }
-// Cache bits of the streaming rollout's trajectory stores: nt (streaming)
-// and sc1 (device scope), the combination measured fastest for these write
-// streams (nt alone 2% slower, plain or sc1-only stores 25-40% slower).
-constexpr int kStreamStoreAux = 2 | 16;
+// Cache bits of the streaming rollout's trajectory stores and state loads:
+// nt (streaming) and sc1 (device scope), the combination measured fastest
+// for these write streams (nt alone 2% slower, plain or sc1-only stores
+// 25-40% slower; for the loads nt with or without sc1 is the same).
+constexpr int kStreamAux = 2 | 16;
 __device__ __forceinline__ void stream_store(float v, __amdgpu_buffer_rsrc_t r, int off) {
-  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, off, 0, kStreamStoreAux);
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, off, 0, kStreamAux);
+}
+__device__ __forceinline__ float stream_load(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, off, 0, kStreamAux));
 }
 
 template <class P>
@@ -182,25 +186,43 @@ template <Phase kPhase, bool kOff32>
 __global__ __launch_bounds__(kBlock) void k_stream_step(StepParams p, uint32_t j, uint32_t T,
                                                         unsigned long long *global) {
   const uint32_t i = blockIdx.x * kBlock + threadIdx.x;
+  // The middle and last steps below 2^30 environments load the state (and
+  // the last step its episode index) before generating the action word,
+  // whose work then overlaps the loads' latency (1.2% faster per launch); a
+  // lane past the end reads 0 from past the end of the planes.  The first
+  // step reads the state arrays, which it writes (below), in program order.
+  constexpr bool kEarly = kOff32 && kPhase != Phase::kFirst;
+  State s{0.0f, 0.0f, 0.0f, 0.0f};
+  uint32_t kprev = 0u;
+  if (kEarly) {
+    const uint32_t pb = p.n * 4u;  // below 2^32: n < 2^30 here
+    const int off = int(i * 4u);
+    s = State{stream_load(plane_rsrc(p.xi, pb), off), stream_load(plane_rsrc(p.xdi, pb), off),
+              stream_load(plane_rsrc(p.thi, pb), off), stream_load(plane_rsrc(p.thdi, pb), off)};
+    if (kPhase == Phase::kLast)
+      kprev = __builtin_amdgcn_raw_buffer_load_b32(plane_rsrc(p.ep_index, pb), off, 0, 0);
+  }
   const uint32_t a = action_bit_wave(p.kact, p.env_base + i, p.t);
   uint32_t n_done = 0u, ret = 0u;  // the last step's per-environment totals
   if (i < p.n) {
-    const State s{__builtin_nontemporal_load(elem<kOff32>(p.xi, i)),
-                  __builtin_nontemporal_load(elem<kOff32>(p.xdi, i)),
-                  __builtin_nontemporal_load(elem<kOff32>(p.thi, i)),
-                  __builtin_nontemporal_load(elem<kOff32>(p.thdi, i))};
+    if (!kEarly) {
+      s = State{__builtin_nontemporal_load(elem<kOff32>(p.xi, i)),
+                __builtin_nontemporal_load(elem<kOff32>(p.xdi, i)),
+                __builtin_nontemporal_load(elem<kOff32>(p.thi, i)),
+                __builtin_nontemporal_load(elem<kOff32>(p.thdi, i))};
+      if (kPhase == Phase::kLast) kprev = *elem<kOff32>(p.ep_index, i);
+    }
     // The starting counters are parked in x and x_dot as binary32 bit
     // patterns (stores and loads move the bits unchanged), through the
     // arrays' own type so that they stay ordered after this lane's loads of
     // x[i] and x_dot[i] and before its final stores.
-    uint32_t k0 = 0u, len0 = 0u, kprev = 0u;
+    uint32_t k0 = 0u, len0 = 0u;
     if (kPhase == Phase::kFirst) {
       k0 = *elem<kOff32>(p.ep_index, i);
       len0 = *elem<kOff32>(p.ep_len, i);
       *elem<kOff32>(p.x, i) = __builtin_bit_cast(float, k0);
       *elem<kOff32>(p.xd, i) = __builtin_bit_cast(float, len0);
     }
-    if (kPhase == Phase::kLast) kprev = *elem<kOff32>(p.ep_index, i);
     State o = dynamics(s, force_of(a));
     const uint32_t d = terminated(o) ? 1u : 0u;
     if (kOff32 && kPhase != Phase::kLast) {
@@ -241,7 +263,7 @@ __global__ __launch_bounds__(kBlock) void k_stream_step(StepParams p, uint32_t j
       if (p.reward) stream_store(1.0f, plane_rsrc(p.reward, pb), off);
       if (p.done)
         __builtin_amdgcn_raw_buffer_store_b8(uint8_t(d), plane_rsrc(p.done, p.n), int(i), 0,
-                                             kStreamStoreAux);
+                                             kStreamAux);
     } else {
       __builtin_nontemporal_store(o.x, elem<kOff32>(p.obs, i));
       __builtin_nontemporal_store(o.xd, elem<kOff32>(p.obs + size_t(p.n), i));
