@@ -105,21 +105,21 @@ COUNTERS = {
     # rollout's launches (1 first, 98 middle, 1 last)
     "stream_step_16777216": {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_device.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "7e4280278896597c", "fetch_kib": 157590.3, "write_kib": 388467.2, "profile": "profiles/stream_step_16777216x100_hbm.md"},
+        "sha256_16": "59dd7006ab6e90d4", "fetch_kib": 157404.1, "write_kib": 388467.2, "profile": "profiles/stream_step_16777216x100_hbm.md"},
     # HBM traffic of one launch-bound launch (graph-replayed fused step,
     # 65,536 environments): FETCH_SIZE and WRITE_SIZE, KiB per dispatch
     "fused_step_65536": {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_device.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "7e4280278896597c", "fetch_kib": 813.9, "write_kib": 2702.8, "profile": "profiles/fused_step_65536env_trace_and_traffic.md"},
+        "sha256_16": "59dd7006ab6e90d4", "fetch_kib": 813.9, "write_kib": 2702.8, "profile": "profiles/fused_step_65536env_trace_and_traffic.md"},
     # the resident rollout, 1,048,576 x 1,000: SQ_INSTS_VALU per wave-step
     "resident_1048576x1000": {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h", _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "4c72ea17994613a3", "valu_per_wave_step": 67.6, "envs_per_wave": 64, "profile": "profiles/resident_1048576x1000_valu.md"},
+        "sha256_16": "1995cf4999900122", "valu_per_wave_step": 67.6, "envs_per_wave": 64, "profile": "profiles/resident_1048576x1000_valu.md"},
     # the same rollout stepped in binary64 and in binary16 (the binary16 kernel
     # holds two environments per lane: 128 per wave)
     "resident_f64_1048576x1000": {
         "sources": [_CSRC + "cp_step.hip", _CSRC + "cp_resident.h", _CSRC + "cp_device.h", _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
-        "sha256_16": "4c72ea17994613a3", "valu_per_wave_step": 87.6, "envs_per_wave": 64, "profile": "profiles/resident_1048576x1000_valu.md"},
+        "sha256_16": "1995cf4999900122", "valu_per_wave_step": 87.6, "envs_per_wave": 64, "profile": "profiles/resident_1048576x1000_valu.md"},
     "resident_f16_1048576x1000": {
         "sources": [_CSRC + "cp_resident16.hip", _CSRC + "cp_f16_table.h", _CSRC + "cp_resident.h", _CSRC + "cp_device.h", _CSRC + "cp_precision.h", _CSRC + "cp_launch.h"],
         "sha256_16": "45787682f245e01a", "valu_per_wave_step": 71.8, "envs_per_wave": 128, "profile": "profiles/resident_1048576x1000_valu.md"},
