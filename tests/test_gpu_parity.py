@@ -485,6 +485,25 @@ def test_streaming_resume_sharding_and_fused_step_agree(gpu):
     torch.cuda.empty_cache()
 
 
+def test_streaming_with_partial_outputs(gpu):
+    # The streaming rollout writes whichever outputs the caller passes: with
+    # the obs trajectory alone, or with totals but no per-environment
+    # statistics (the last step then sums its statistics into the totals
+    # only), it leaves the same state, counters and outputs as with all.
+    n, T = (1 << 21) + 333, 40
+    full, ftr = run(cp.CP_FUSED, n, T, seed=10)
+    for kw in (dict(reward=False, done=False, stats=False, totals=False),
+               dict(stats=False, totals=True), dict(done=False, stats=True, totals=False)):
+        s, tr = run(cp.CP_FUSED, n, T, seed=10, **kw)
+        assert all(np.array_equal(x, y) for x, y in zip(gpu_state(s), gpu_state(full))), kw
+        for f in ("obs", "reward", "done", "done_count", "total_reward", "ret_sum", "totals"):
+            if getattr(tr, f) is not None:
+                assert torch.equal(getattr(tr, f), getattr(ftr, f)), (kw, f)
+        del s, tr
+    del full, ftr
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("variant", ALL, ids=lambda v: NAMES[v])
 def test_steps_equal_rollout(gpu, variant):
     n, T = 777, 40
